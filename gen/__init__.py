@@ -70,6 +70,10 @@ def cpu_lib():
                                         ctypes.c_uint32, ctypes.c_int32, ctypes.c_uint64, ctypes.c_int64,
                                         ctypes.c_void_p]
         L.gen_fill_rows_cpu.restype = ctypes.c_int
+        L.gen_fill_rows_list_cpu.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64,
+                                             ctypes.c_uint32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
+                                             ctypes.c_void_p]
+        L.gen_fill_rows_list_cpu.restype = ctypes.c_int
         L.gen_priorities.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                                      ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int64,
                                      ctypes.c_void_p]
@@ -122,6 +126,17 @@ def fill_rows_cpu(col, col_id, seed, T, k0, nrows):
                                      out.ctypes.data)
     if st != 0:
         raise ValueError("gen_fill_rows_cpu rejected its arguments")
+    return out
+
+
+def fill_rows_list_cpu(col, col_id, seed, T, ks):
+    """Rows of the insertions listed in ks, as uint8 [len(ks), T*E]."""
+    ks = np.ascontiguousarray(ks, dtype=np.uint64)
+    out = np.empty((ks.size, T * col.elem_bytes), dtype=np.uint8)
+    st = cpu_lib().gen_fill_rows_list_cpu(col.kind, col.param, col.m, seed, col_id, T, ks.ctypes.data,
+                                          ks.size, out.ctypes.data)
+    if st != 0:
+        raise ValueError("gen_fill_rows_list_cpu rejected its arguments")
     return out
 
 

@@ -253,3 +253,17 @@ int gen_priorities(int dist, double a, double b, double c, uint64_t seed, uint32
     }
     return 0;
 }
+
+/* Rows for an arbitrary list of insertion numbers ks[0..n) into
+ * out[n][T][m * elem_size]: row i is the row of insertion ks[i]. */
+int gen_fill_rows_list_cpu(int kind, int64_t param, int32_t m, uint64_t seed, uint32_t col,
+                           int32_t T, const uint64_t *ks, int64_t n, uint8_t *out)
+{
+    int64_t i;
+    int64_t row_bytes = (int64_t)T * m * gen_elem_size(kind);
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+    for (i = 0; i < n; i++)
+        bad |= gen_fill_rows_cpu(kind, param, m, seed, col, T, ks[i], 1, out + i * row_bytes) != 0;
+    return bad ? -1 : 0;
+}

@@ -1,0 +1,221 @@
+/*
+ * gear.h - C ABI of the MI355X (gfx950) experience-replay library.
+ *
+ * The library keeps a fixed-capacity store of trajectories as column tables
+ * and runs the data-parallel hot path of GPU-centric experience replay
+ * (GEAR, Wang et al., arXiv 2310.05205) on one GPU:
+ *   selection  - FIFO / LIFO / uniform / prioritized (prefix scan over the
+ *                priorities, then one search per uniform draw),
+ *                importance-sampling weights, priority-update scatter;
+ *   collection - gather of fixed-length windows of selected trajectories
+ *                into contiguous per-column batches, from a table held in
+ *                HBM or in pinned host memory read zero-copy by the kernel.
+ *
+ * Conventions for every call:
+ *   - Return value: GEAR_OK (0) or a negative GEAR_E_* code.  A failing call
+ *     enqueues nothing and leaves the table unchanged; gear_last_error()
+ *     then returns a message for the calling thread.
+ *   - `stream` is a hipStream_t passed as void*; NULL means the null stream.
+ *     Every device-side effect is enqueued on `stream` and is asynchronous
+ *     to the host; only gear_table_sync() blocks.
+ *   - Pointers named d_* are device memory (hipMalloc, or a torch CUDA
+ *     tensor's data pointer) on the table's device.  They are owned by the
+ *     caller and must stay valid until the enqueued work has completed.
+ *   - A table is not thread-safe.  All calls on one table must be ordered:
+ *     issue them from one host thread, on one stream, or order the streams
+ *     with events.  Separate tables are independent.
+ *   - Conditions only the device can see (all priorities zero, an index or
+ *     window start out of range) are recorded in the table's device status
+ *     word, returned and cleared by gear_table_sync().
+ */
+#ifndef GEAR_H
+#define GEAR_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define GEAR_OK              0
+#define GEAR_E_INVAL        -1   /* invalid argument (null pointer, size out of range, ...) */
+#define GEAR_E_NOMEM        -2   /* device or pinned host allocation failed */
+#define GEAR_E_EMPTY        -3   /* selection from a table with nothing inserted */
+#define GEAR_E_INSUFFICIENT -4   /* FIFO/LIFO asked for more trajectories than are live */
+#define GEAR_E_HIP          -5   /* a HIP runtime call or kernel launch failed */
+
+/* Bits of the device status word (gear_table_sync). */
+#define GEAR_STATUS_NO_WEIGHT  1u  /* prioritized select saw a priority total of 0 */
+#define GEAR_STATUS_BAD_INDEX  2u  /* collect/update saw an index or start out of range */
+#define GEAR_STATUS_INTERNAL   4u  /* a kernel's bounded wait expired (library defect) */
+
+/* Where the column tables live. */
+#define GEAR_DEVICE       0  /* HBM of the table's GPU */
+#define GEAR_HOST_PINNED  1  /* page-locked host memory, mapped and read zero-copy by kernels */
+
+/* Selection strategies (GEAR Sec. 1 list of strategies; Sec. 3.3). */
+#define GEAR_FIFO         0
+#define GEAR_LIFO         1
+#define GEAR_UNIFORM      2
+#define GEAR_PRIORITIZED  3
+
+/* Limits. */
+#define GEAR_MAX_CAPACITY  (1ll << 30)  /* keeps every priority total below 2^62 */
+#define GEAR_MAX_COLUMNS   64
+#define GEAR_MAX_BATCH     (1 << 24)
+
+typedef struct gear_table gear_table;
+
+/*
+ * gear_table_create - allocate an empty store (Sec. 3.2, shard storage
+ * format: one column table per field type, each a contiguous array of
+ * `capacity` equal blocks; a block holds one field of one trajectory as T
+ * steps of elem_bytes[c] bytes; all tables share the capacity).
+ *
+ *   elem_bytes  host array of ncols sizes, bytes per step of each column (>= 1)
+ *   ncols       0 .. GEAR_MAX_COLUMNS (0 gives a selection-only store)
+ *   capacity    number of trajectory slots N, 1 .. GEAR_MAX_CAPACITY
+ *   T           steps per trajectory, >= 1
+ *   residency   GEAR_DEVICE or GEAR_HOST_PINNED
+ *   device      HIP device ordinal that runs the kernels
+ *   out         receives the table handle
+ *
+ * Column c is laid out as [capacity][T][elem_bytes[c]] bytes.  The store
+ * also owns the uint32 priority array [capacity] (zero = not selectable,
+ * Sec. 3.2 index manager) in HBM, and the scan, search and scatter scratch,
+ * all sized by `capacity` at creation; no later call allocates.
+ * Errors: GEAR_E_INVAL, GEAR_E_NOMEM, GEAR_E_HIP.
+ */
+int gear_table_create(const int64_t *elem_bytes, int32_t ncols, int64_t capacity, int32_t T,
+                      int32_t residency, int32_t device, gear_table **out);
+
+/* gear_table_destroy - synchronize the table's device and free all its
+ * memory.  NULL is accepted.  Errors: GEAR_E_HIP. */
+int gear_table_destroy(gear_table *t);
+
+/*
+ * gear_insert - append n trajectories with FIFO removal (Sec. 3.2, insertion
+ * and deletion: once the store is full the oldest trajectory is the
+ * victim).  Insertion number k (counted from 0 over the table's life) is
+ * written to slot k mod capacity; when n > capacity only the last
+ * `capacity` rows are kept, as if written one after another.
+ *
+ *   n           number of rows, >= 0
+ *   col_src     host array of ncols pointers; col_src[c] holds n*T*elem_bytes[c]
+ *               bytes ([n][T][elem_bytes[c]]), host or device memory
+ *               (may be NULL when ncols == 0)
+ *   priorities  n uint32 values, host or device memory; 0 inserts an
+ *               unselectable trajectory
+ *
+ * Copies are enqueued on `stream`; sources must stay valid until they
+ * complete.  Updates the host-side insertion count at once.
+ * Errors: GEAR_E_INVAL, GEAR_E_HIP.
+ */
+int gear_insert(gear_table *t, int64_t n, const void *const *col_src, const uint32_t *priorities,
+                void *stream);
+
+/*
+ * gear_select - choose B trajectories and an L-step window in each (Sec. 1
+ * strategies; Sec. 3.3 centralized selection: weighted sampling is a prefix
+ * sum over the weights followed by a binary search for each uniformly drawn
+ * number; Sec. 3.2: items with priority zero are never selected).
+ *
+ *   strategy  GEAR_FIFO: the B oldest live trajectories, oldest first.
+ *             GEAR_LIFO: the B newest, newest first.
+ *             GEAR_UNIFORM: B draws with replacement, uniform over live slots.
+ *             GEAR_PRIORITIZED: B draws with replacement, slot i with
+ *             probability p_i / S, S the sum of all priorities.
+ *   B         1 .. GEAR_MAX_BATCH (FIFO/LIFO: at most the live count)
+ *   L         window length in steps, 1 .. T
+ *   seed      draw b uses splitmix64 outputs 2b (index) and 2b+1 (start) of
+ *             the stream seeded with `seed`; a draw is floor(u * n / 2^64)
+ *   beta      importance-sampling exponent (used only when d_weights != NULL)
+ *   d_idx     out, int64[B]: selected slot per draw
+ *   d_start   out, int32[B]: window start, uniform on [0, T-L]
+ *   d_weights out, float[B] or NULL: prioritized: (n*P(i))^-beta normalised
+ *             by the batch maximum (n = live count); other strategies: 1
+ *
+ * A prioritized select rescans the priorities only if an insert or update
+ * changed them since the last scan.  If all priorities are zero the device
+ * writes idx = -1, start = 0, weight = 0 and sets GEAR_STATUS_NO_WEIGHT.
+ * Errors: GEAR_E_INVAL, GEAR_E_EMPTY (nothing inserted), GEAR_E_INSUFFICIENT,
+ * GEAR_E_HIP.
+ */
+int gear_select(gear_table *t, int32_t strategy, int32_t B, int32_t L, uint64_t seed, float beta,
+                int64_t *d_idx, int32_t *d_start, float *d_weights, void *stream);
+
+/*
+ * gear_collect - gather L consecutive steps of the requested columns of each
+ * selected trajectory into contiguous batches (Sec. 3.2: a client reads a
+ * range of timesteps of a subset of fields; Sec. 3.4: one collection kernel
+ * reads the selected blocks of each requested table, from pinned host memory
+ * without a CPU copy).  For draw b, step t < L and requested column j:
+ *     out[j][b][t][:] = column col_ids[j], slot d_idx[b], step d_start[b] + t
+ *
+ *   d_idx, d_start  device int64[B], int32[B] (as written by gear_select)
+ *   B, L            1 .. GEAR_MAX_BATCH, 1 .. T
+ *   col_ids         host int32[ncols] column numbers, or NULL for all columns
+ *   ncols           number of requested columns (table's ncols when col_ids is NULL)
+ *   d_out           host array of ncols device pointers; d_out[j] receives
+ *                   B*L*elem_bytes[col_ids[j]] bytes laid out [B][L][elem_bytes]
+ *
+ * A draw whose index lies outside [0, capacity) or whose start lies outside
+ * [0, T-L] gets zero bytes and sets GEAR_STATUS_BAD_INDEX.
+ * Errors: GEAR_E_INVAL, GEAR_E_HIP.
+ */
+int gear_collect(gear_table *t, const int64_t *d_idx, const int32_t *d_start, int32_t B, int32_t L,
+                 const int32_t *col_ids, int32_t ncols, void *const *d_out, void *stream);
+
+/*
+ * gear_update_priorities - write new priorities for selected slots (Sec. 3.2:
+ * the status table holds the priorities; updates are consolidated and
+ * committed).  Applied as if in batch order: when a slot appears more than
+ * once, the last occurrence's value wins.
+ *
+ *   d_idx            device int64[B], slots in [0, live count)
+ *   d_new_priorities device uint32[B]
+ *   B                0 .. GEAR_MAX_BATCH
+ *
+ * An index outside [0, live count) is skipped and sets GEAR_STATUS_BAD_INDEX.
+ * Errors: GEAR_E_INVAL, GEAR_E_HIP.
+ */
+int gear_update_priorities(gear_table *t, const int64_t *d_idx, const uint32_t *d_new_priorities,
+                           int32_t B, void *stream);
+
+/*
+ * gear_table_sync - wait for `stream`, then read and clear the device status
+ * word.  *device_status (may be NULL) receives the GEAR_STATUS_* bits set
+ * since the previous sync.  The only blocking call.
+ * Errors: GEAR_E_INVAL, GEAR_E_HIP.
+ */
+int gear_table_sync(gear_table *t, void *stream, int32_t *device_status);
+
+/* gear_table_info - host-side ring state: live count min(next_seq, capacity)
+ * and the number of insertions so far.  Either output may be NULL. */
+int gear_table_info(const gear_table *t, int64_t *count, uint64_t *next_seq);
+
+/*
+ * gear_table_column - base address of column c ([capacity][T][elem_bytes]):
+ * a device pointer for GEAR_DEVICE tables, a device-accessible mapped
+ * pointer for GEAR_HOST_PINNED ones; *host_ptr receives the host-side
+ * address of a pinned table (NULL for device tables).  Writing through it
+ * is the in-place insertion path (Sec. 3.2, allocate/commit); the caller
+ * orders such writes with the table's stream.  Any output may be NULL.
+ */
+int gear_table_column(const gear_table *t, int32_t c, void **base, void **host_ptr,
+                      int64_t *elem_bytes);
+
+/* gear_table_priorities - device pointer of the uint32 priority array
+ * [capacity].  Reading it is safe after the stream work that wrote it. */
+int gear_table_priorities(const gear_table *t, uint32_t **d_priority);
+
+/* gear_last_error - message describing the last failed call on this
+ * thread ("" if none).  Valid until the next call on the same thread. */
+const char *gear_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GEAR_H */

@@ -1,0 +1,243 @@
+// Window collection on gfx950 (GEAR Sec. 3.2 storage format; Sec. 3.4).
+//
+// For draw b, step t < L and requested column j:
+//     out_j[b][t][:] = column c_j, block idx[b], step start[b] + t
+// Each window is one contiguous byte range of its column,
+//     base_c + (idx[b]*T + start[b]) * E_c,  length W_c = L * E_c,
+// and each column's batch [B][L][E_c] is one contiguous range, so the copy
+// is driven by the output: a workgroup owns a contiguous piece of one
+// column's output.  Wide windows (W_c at least a piece) are split into
+// pieces; narrow windows are packed several to a piece with their source
+// offsets staged in LDS.  All requested columns run in one launch.  A column
+// table in pinned host memory is read by the same kernel through its mapped
+// address, so the loads go over the host link without a CPU copy.
+//
+// Element width per column: 16 bytes when every window source and output
+// address is 16-byte aligned, else 4 bytes when 4-byte aligned, else 1.
+#include "gear_internal.h"
+
+namespace gear {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 4;          // elements in flight per thread
+constexpr int kMaxLaunchCols = 16;  // columns per launch (more take several launches)
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+struct ColTask {
+    const uint8_t* src;   // device-visible column base
+    uint8_t* out;         // batch output [B][W]
+    int64_t E;            // bytes per step
+    int64_t W;            // window bytes, L*E
+    int64_t task0;        // first task (workgroup) of this column
+    int64_t piece;        // bytes per piece: kThreads * kUnroll * width
+    int64_t ppw;          // pieces per window (wide columns)
+    int32_t width;        // element bytes: 16, 4 or 1
+    int32_t wide;         // 1: pieces of one window; 0: several windows per piece
+    int32_t wpp;          // windows per piece (narrow)
+    uint32_t epw;         // elements per window (narrow)
+    uint32_t magic;       // ceil(2^32 / epw) for epw > 1: exact quotient for operands < 2^16
+};
+
+struct CollectArgs {
+    ColTask col[kMaxLaunchCols];
+    int32_t ncols;
+    const int64_t* idx;
+    const int32_t* start;
+    int32_t B;
+    int32_t T;
+    int32_t L;
+    int64_t N;
+    uint32_t* status;
+};
+
+template <int WIDTH>
+struct Elem;
+template <>
+struct Elem<16> {
+    typedef u32x4 type;
+};
+template <>
+struct Elem<4> {
+    typedef uint32_t type;
+};
+template <>
+struct Elem<1> {
+    typedef uint8_t type;
+};
+
+// Streaming loads: table bytes are read once per collection.
+template <int WIDTH>
+__device__ inline typename Elem<WIDTH>::type load_stream(const typename Elem<WIDTH>::type* p) {
+    return __builtin_nontemporal_load(p);
+}
+
+template <int WIDTH>
+__device__ inline typename Elem<WIDTH>::type zero_elem() {
+    return typename Elem<WIDTH>::type(0);
+}
+
+// Validated source byte offset of window b's first step, or -1.
+__device__ inline int64_t window_offset(const CollectArgs& a, const ColTask& c, int64_t b) {
+    const int64_t i = a.idx[b];
+    const int32_t s = a.start[b];
+    if (i < 0 || i >= a.N || s < 0 || s > a.T - a.L) return -1;
+    return (i * a.T + s) * c.E;
+}
+
+template <int WIDTH>
+__device__ void copy_wide(const CollectArgs& a, const ColTask& c, int64_t q) {
+    typedef typename Elem<WIDTH>::type V;
+    const int64_t b = q / c.ppw;
+    const int64_t off0 = (q - b * c.ppw) * c.piece;
+    const int64_t len = (c.W - off0) < c.piece ? (c.W - off0) : c.piece;
+    const int64_t n = len / WIDTH;
+    V* dst = reinterpret_cast<V*>(c.out + b * c.W + off0);
+    const int64_t so = window_offset(a, c, b);
+    if (so < 0) {
+        for (int64_t e = threadIdx.x; e < n; e += kThreads) dst[e] = zero_elem<WIDTH>();
+        if (threadIdx.x == 0) atomicOr(a.status, GEAR_STATUS_BAD_INDEX);
+        return;
+    }
+    const V* src = reinterpret_cast<const V*>(c.src + so + off0);
+    if (n == (int64_t)kThreads * kUnroll) {
+        V v[kUnroll];
+#pragma unroll
+        for (int k = 0; k < kUnroll; k++) v[k] = load_stream<WIDTH>(src + threadIdx.x + k * kThreads);
+#pragma unroll
+        for (int k = 0; k < kUnroll; k++) dst[threadIdx.x + k * kThreads] = v[k];
+    } else {
+        for (int64_t e = threadIdx.x; e < n; e += kThreads) dst[e] = load_stream<WIDTH>(src + e);
+    }
+}
+
+template <int WIDTH>
+__device__ void copy_narrow(const CollectArgs& a, const ColTask& c, int64_t q) {
+    typedef typename Elem<WIDTH>::type V;
+    __shared__ int64_t s_off[kThreads];   // source element offset per window, -1 if invalid
+    __shared__ int s_bad;
+    const int64_t b0 = q * c.wpp;
+    const int nb = (int)((a.B - b0) < c.wpp ? (a.B - b0) : c.wpp);
+    if (threadIdx.x == 0) s_bad = 0;
+    __syncthreads();
+    if ((int)threadIdx.x < nb) {
+        const int64_t so = window_offset(a, c, b0 + threadIdx.x);
+        s_off[threadIdx.x] = so < 0 ? -1 : so / WIDTH;
+        if (so < 0) s_bad = 1;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0 && s_bad) atomicOr(a.status, GEAR_STATUS_BAD_INDEX);
+    const uint32_t total = (uint32_t)nb * c.epw;
+    const V* src = reinterpret_cast<const V*>(c.src);
+    V* dst = reinterpret_cast<V*>(c.out) + b0 * (int64_t)c.epw;
+    V v[kUnroll];
+#pragma unroll
+    for (int k = 0; k < kUnroll; k++) {
+        const uint32_t e = threadIdx.x + k * kThreads;
+        v[k] = zero_elem<WIDTH>();
+        if (e < total) {
+            const uint32_t w = c.epw == 1 ? e : __umulhi(e, c.magic);
+            const int64_t so = s_off[w];
+            if (so >= 0) v[k] = load_stream<WIDTH>(src + so + (e - w * c.epw));
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < kUnroll; k++) {
+        const uint32_t e = threadIdx.x + k * kThreads;
+        if (e < total) dst[e] = v[k];
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void collect_kernel(CollectArgs a) {
+    const int64_t task = blockIdx.x;
+    int j = 0;
+    while (j + 1 < a.ncols && a.col[j + 1].task0 <= task) j++;
+    const ColTask& c = a.col[j];
+    const int64_t q = task - c.task0;
+    if (c.wide) {
+        if (c.width == 16) copy_wide<16>(a, c, q);
+        else if (c.width == 4) copy_wide<4>(a, c, q);
+        else copy_wide<1>(a, c, q);
+    } else {
+        if (c.width == 16) copy_narrow<16>(a, c, q);
+        else if (c.width == 4) copy_narrow<4>(a, c, q);
+        else copy_narrow<1>(a, c, q);
+    }
+}
+
+}  // namespace
+}  // namespace gear
+
+using gear::fail;
+using gear::hip_fail;
+
+extern "C" int gear_collect(gear_table* h, const int64_t* d_idx, const int32_t* d_start, int32_t B, int32_t L,
+                            const int32_t* col_ids, int32_t ncols, void* const* d_out, void* stream) {
+    if (h == nullptr) return fail(GEAR_E_INVAL, "gear_collect: table is NULL");
+    gear::Table* t = reinterpret_cast<gear::Table*>(h);
+    if (B < 1 || B > GEAR_MAX_BATCH) return fail(GEAR_E_INVAL, "gear_collect: B out of range");
+    if (L < 1 || L > t->T) return fail(GEAR_E_INVAL, "gear_collect: L must lie in [1, T]");
+    if (d_idx == nullptr || d_start == nullptr || d_out == nullptr)
+        return fail(GEAR_E_INVAL, "gear_collect: NULL pointer argument");
+    if (col_ids == nullptr && ncols != t->ncols)
+        return fail(GEAR_E_INVAL, "gear_collect: ncols must equal the table's column count when col_ids is NULL");
+    if (ncols < 1 || ncols > GEAR_MAX_COLUMNS) return fail(GEAR_E_INVAL, "gear_collect: ncols out of range");
+    for (int j = 0; j < ncols; j++) {
+        const int c = col_ids ? col_ids[j] : j;
+        if (c < 0 || c >= t->ncols) return fail(GEAR_E_INVAL, "gear_collect: no such column");
+        if (d_out[j] == nullptr) return fail(GEAR_E_INVAL, "gear_collect: output pointer is NULL");
+    }
+    gear::DeviceGuard guard(t->device);
+    if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_collect: hipSetDevice");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    for (int j0 = 0; j0 < ncols; j0 += gear::kMaxLaunchCols) {
+        gear::CollectArgs a{};
+        a.idx = d_idx;
+        a.start = d_start;
+        a.B = B;
+        a.T = t->T;
+        a.L = L;
+        a.N = t->N;
+        a.status = t->status;
+        a.ncols = 0;
+        int64_t tasks = 0;
+        for (int j = j0; j < ncols && j < j0 + gear::kMaxLaunchCols; j++) {
+            const int c = col_ids ? col_ids[j] : j;
+            gear::ColTask& ct = a.col[a.ncols++];
+            ct.src = t->col_dev[c];
+            ct.out = static_cast<uint8_t*>(d_out[j]);
+            ct.E = t->elem_bytes[c];
+            ct.W = (int64_t)L * ct.E;
+            const uintptr_t sa = reinterpret_cast<uintptr_t>(ct.src), oa = reinterpret_cast<uintptr_t>(ct.out);
+            if (ct.E % 16 == 0 && sa % 16 == 0 && oa % 16 == 0) ct.width = 16;
+            else if (ct.E % 4 == 0 && sa % 4 == 0 && oa % 4 == 0) ct.width = 4;
+            else ct.width = 1;
+            ct.piece = (int64_t)gear::kThreads * gear::kUnroll * ct.width;
+            ct.task0 = tasks;
+            if (ct.W >= ct.piece) {
+                ct.wide = 1;
+                ct.ppw = (ct.W + ct.piece - 1) / ct.piece;
+                ct.wpp = 1;
+                ct.epw = 0;
+                ct.magic = 0;
+                tasks += (int64_t)B * ct.ppw;
+            } else {
+                ct.wide = 0;
+                ct.ppw = 1;
+                int64_t wpp = ct.piece / ct.W;
+                if (wpp > gear::kThreads) wpp = gear::kThreads;
+                ct.wpp = (int32_t)wpp;
+                ct.epw = (uint32_t)(ct.W / ct.width);
+                ct.magic = ct.epw > 1 ? (uint32_t)(((1ull << 32) + ct.epw - 1) / ct.epw) : 0u;
+                tasks += (B + wpp - 1) / wpp;
+            }
+        }
+        if (tasks > 0x7FFFFFFF) return fail(GEAR_E_INVAL, "gear_collect: batch too large for one launch");
+        hipLaunchKernelGGL(gear::collect_kernel, dim3((unsigned)tasks), dim3(gear::kThreads), 0, s, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, "gear_collect: launch");
+    }
+    return GEAR_OK;
+}

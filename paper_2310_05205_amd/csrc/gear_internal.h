@@ -1,0 +1,81 @@
+// Internal declarations of the gfx950 experience-replay library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "gear.h"
+
+namespace gear {
+
+// Priority scan geometry.  A tile is 256 priorities: one wave64, four per
+// lane, one 16-byte load per lane.  A chunk (one workgroup of the scan) is
+// 16 tiles.  The search descends a tree of inclusive prefix sums with fan-out
+// 256: level 0 holds the prefix at the end of every tile, level l the prefix
+// at the end of every 256^l tiles; the top level has at most 256 entries.
+constexpr int kTile = 256;
+constexpr int kTilesPerChunk = 16;
+constexpr int kChunk = kTile * kTilesPerChunk;
+constexpr int kFanout = 256;
+constexpr int kMaxLevels = 6;
+
+struct Table {
+    int device = 0;
+    int residency = GEAR_DEVICE;
+    int64_t N = 0;
+    int32_t T = 0;
+    int32_t ncols = 0;
+    std::vector<int64_t> elem_bytes;
+    std::vector<uint8_t*> col_dev;    // device-visible base of each column
+    std::vector<uint8_t*> col_host;   // host base (pinned tables), else null
+
+    uint64_t next_seq = 0;            // insertions so far (host-side ring state)
+
+    uint32_t* priority = nullptr;     // [N]
+    uint32_t* tag = nullptr;          // [N] scatter winner tags, kept zero between calls
+
+    // Scan / search state.
+    int64_t ntiles = 0, nchunks = 0;
+    int nlevels = 0;                  // levels of the prefix tree (level 0 = per tile)
+    int64_t level_size[kMaxLevels] = {};
+    uint64_t* level[kMaxLevels] = {};
+    uint64_t* lookback = nullptr;     // [2][nchunks] packed (state, value) words
+    uint32_t* ticket = nullptr;       // [2] chunk tickets, double-buffered
+    unsigned long long* pmin = nullptr;  // batch minimum priority, epoch-tagged
+    uint32_t* status = nullptr;       // device status word
+    int scan_parity = 0;
+    bool cdf_dirty = true;
+    uint32_t select_epoch = 0;
+};
+
+// Thread-local error reporting.
+int fail(int code, const std::string& msg);
+int hip_fail(hipError_t e, const char* what);
+
+// Makes the table's device current for the lifetime of the guard.
+class DeviceGuard {
+  public:
+    explicit DeviceGuard(int dev);
+    ~DeviceGuard();
+    hipError_t error() const { return err_; }
+
+  private:
+    int prev_ = -1;
+    hipError_t err_ = hipSuccess;
+};
+
+// Kernel launchers (each returns hipSuccess or the launch error).
+hipError_t launch_scan(Table& t, hipStream_t s);
+hipError_t launch_search(Table& t, int32_t B, int32_t L, uint64_t seed, bool want_min,
+                         int64_t* idx, int32_t* start, hipStream_t s);
+hipError_t launch_is_weights(Table& t, int32_t B, float beta, const int64_t* idx, float* w,
+                             hipStream_t s);
+hipError_t launch_simple_select(Table& t, int32_t strategy, int32_t B, int32_t L, uint64_t seed,
+                                int64_t* idx, int32_t* start, float* w, hipStream_t s);
+hipError_t launch_scatter(Table& t, const int64_t* idx, const uint32_t* newp, int32_t B,
+                          hipStream_t s);
+
+}  // namespace gear

@@ -1,0 +1,276 @@
+// Host runtime of the replay store: creation, insertion with FIFO removal,
+// status synchronisation and accessors (GEAR Sec. 3.2).
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "gear_internal.h"
+
+namespace gear {
+
+namespace {
+thread_local std::string g_last_error;
+}
+
+int fail(int code, const std::string& msg) {
+    g_last_error = msg;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    std::string m = what;
+    m += ": ";
+    m += hipGetErrorString(e);
+    return fail(GEAR_E_HIP, m);
+}
+
+DeviceGuard::DeviceGuard(int dev) {
+    int cur = -1;
+    err_ = hipGetDevice(&cur);
+    if (err_ == hipSuccess && cur != dev) {
+        err_ = hipSetDevice(dev);
+        if (err_ == hipSuccess) prev_ = cur;
+    }
+}
+
+DeviceGuard::~DeviceGuard() {
+    if (prev_ >= 0) (void)hipSetDevice(prev_);
+}
+
+}  // namespace gear
+
+using gear::fail;
+using gear::hip_fail;
+using gear::Table;
+
+namespace {
+
+void free_table(Table* t) {
+    if (!t) return;
+    for (int c = 0; c < t->ncols; c++) {
+        if (t->residency == GEAR_HOST_PINNED) {
+            if (t->col_host[c]) (void)hipHostFree(t->col_host[c]);
+        } else if (t->col_dev[c]) {
+            (void)hipFree(t->col_dev[c]);
+        }
+    }
+    (void)hipFree(t->priority);
+    (void)hipFree(t->tag);
+    for (int l = 0; l < gear::kMaxLevels; l++) (void)hipFree(t->level[l]);
+    (void)hipFree(t->lookback);
+    (void)hipFree(t->ticket);
+    (void)hipFree(t->pmin);
+    (void)hipFree(t->status);
+    delete t;
+}
+
+template <typename P>
+hipError_t dmalloc(P** p, size_t bytes) {
+    return hipMalloc(reinterpret_cast<void**>(p), bytes);
+}
+
+}  // namespace
+
+extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64_t capacity, int32_t T,
+                                 int32_t residency, int32_t device, gear_table** out) {
+    if (out == nullptr) return fail(GEAR_E_INVAL, "gear_table_create: out is NULL");
+    *out = nullptr;
+    if (ncols < 0 || ncols > GEAR_MAX_COLUMNS) return fail(GEAR_E_INVAL, "gear_table_create: ncols out of range");
+    if (ncols > 0 && elem_bytes == nullptr) return fail(GEAR_E_INVAL, "gear_table_create: elem_bytes is NULL");
+    if (capacity < 1 || capacity > GEAR_MAX_CAPACITY) return fail(GEAR_E_INVAL, "gear_table_create: capacity out of range");
+    if (T < 1) return fail(GEAR_E_INVAL, "gear_table_create: T must be >= 1");
+    if (residency != GEAR_DEVICE && residency != GEAR_HOST_PINNED)
+        return fail(GEAR_E_INVAL, "gear_table_create: unknown residency");
+    for (int c = 0; c < ncols; c++) {
+        if (elem_bytes[c] < 1 || elem_bytes[c] > (1ll << 30))
+            return fail(GEAR_E_INVAL, "gear_table_create: elem_bytes out of range");
+        // Column bytes must fit in int64 with room for offsets.
+        if ((double)capacity * (double)T * (double)elem_bytes[c] > 9.0e18)
+            return fail(GEAR_E_INVAL, "gear_table_create: column too large");
+    }
+    if (device < 0) return fail(GEAR_E_INVAL, "gear_table_create: negative device");
+    int ndev = 0;
+    hipError_t e = hipGetDeviceCount(&ndev);
+    if (e != hipSuccess) return hip_fail(e, "gear_table_create: hipGetDeviceCount");
+    if (device >= ndev) return fail(GEAR_E_INVAL, "gear_table_create: no such device");
+    gear::DeviceGuard guard(device);
+    if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_table_create: hipSetDevice");
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, device);
+    if (e != hipSuccess) return hip_fail(e, "gear_table_create: hipGetDeviceProperties");
+    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(GEAR_E_INVAL, std::string("gear_table_create: library is built for gfx950, device is ") + prop.gcnArchName);
+
+    Table* t = new Table();
+    t->device = device;
+    t->residency = residency;
+    t->N = capacity;
+    t->T = T;
+    t->ncols = ncols;
+    t->elem_bytes.assign(elem_bytes, elem_bytes + ncols);
+    t->col_dev.assign(ncols, nullptr);
+    t->col_host.assign(ncols, nullptr);
+
+    auto oom = [&](const char* what, hipError_t err) {
+        free_table(t);
+        std::string m = std::string("gear_table_create: allocation of ") + what + " failed: " + hipGetErrorString(err);
+        return fail(GEAR_E_NOMEM, m);
+    };
+
+    for (int c = 0; c < ncols; c++) {
+        size_t bytes = (size_t)capacity * (size_t)T * (size_t)elem_bytes[c];
+        if (residency == GEAR_DEVICE) {
+            e = hipMalloc(reinterpret_cast<void**>(&t->col_dev[c]), bytes);
+            if (e != hipSuccess) return oom("a device column", e);
+            // Slots never inserted read as zeros, as pinned host pages do.
+            e = hipMemsetAsync(t->col_dev[c], 0, bytes, nullptr);
+            if (e != hipSuccess) {
+                free_table(t);
+                return hip_fail(e, "gear_table_create: clearing a device column");
+            }
+        } else {
+            // Page-locked, mapped into the GPU's address space.  Coarse-grained
+            // (non-coherent) so the GPU may cache lines it reads; the table is
+            // only written by insertion, ordered on the stream.
+            void* h = nullptr;
+            e = hipHostMalloc(&h, bytes, hipHostMallocMapped | hipHostMallocNonCoherent);
+            if (e != hipSuccess) return oom("a pinned host column", e);
+            t->col_host[c] = static_cast<uint8_t*>(h);
+            void* d = nullptr;
+            e = hipHostGetDevicePointer(&d, h, 0);
+            if (e != hipSuccess) return oom("a device view of a pinned column", e);
+            t->col_dev[c] = static_cast<uint8_t*>(d);
+        }
+    }
+
+    // Prefix tree geometry.
+    t->ntiles = (capacity + gear::kTile - 1) / gear::kTile;
+    t->nchunks = (t->ntiles + gear::kTilesPerChunk - 1) / gear::kTilesPerChunk;
+    int64_t sz = t->ntiles;
+    t->nlevels = 0;
+    while (true) {
+        t->level_size[t->nlevels] = sz;
+        t->nlevels++;
+        if (sz <= gear::kFanout) break;
+        sz = (sz + gear::kFanout - 1) / gear::kFanout;
+    }
+    if ((e = dmalloc(&t->priority, sizeof(uint32_t) * capacity)) != hipSuccess) return oom("priorities", e);
+    if ((e = dmalloc(&t->tag, sizeof(uint32_t) * capacity)) != hipSuccess) return oom("scatter tags", e);
+    for (int l = 0; l < t->nlevels; l++)
+        if ((e = dmalloc(&t->level[l], sizeof(uint64_t) * t->level_size[l])) != hipSuccess) return oom("prefix levels", e);
+    if ((e = dmalloc(&t->lookback, sizeof(uint64_t) * 2 * t->nchunks)) != hipSuccess) return oom("look-back words", e);
+    if ((e = dmalloc(&t->ticket, sizeof(uint32_t) * 2)) != hipSuccess) return oom("tickets", e);
+    if ((e = dmalloc(&t->pmin, sizeof(unsigned long long))) != hipSuccess) return oom("batch minimum", e);
+    if ((e = dmalloc(&t->status, sizeof(uint32_t))) != hipSuccess) return oom("status word", e);
+
+    if ((e = hipMemset(t->priority, 0, sizeof(uint32_t) * capacity)) != hipSuccess ||
+        (e = hipMemset(t->tag, 0, sizeof(uint32_t) * capacity)) != hipSuccess ||
+        (e = hipMemset(t->lookback, 0, sizeof(uint64_t) * 2 * t->nchunks)) != hipSuccess ||
+        (e = hipMemset(t->ticket, 0, sizeof(uint32_t) * 2)) != hipSuccess ||
+        (e = hipMemset(t->pmin, 0xFF, sizeof(unsigned long long))) != hipSuccess ||
+        (e = hipMemset(t->status, 0, sizeof(uint32_t))) != hipSuccess ||
+        (e = hipDeviceSynchronize()) != hipSuccess) {
+        free_table(t);
+        return hip_fail(e, "gear_table_create: initialising table state");
+    }
+    *out = reinterpret_cast<gear_table*>(t);
+    return GEAR_OK;
+}
+
+extern "C" int gear_table_destroy(gear_table* h) {
+    if (h == nullptr) return GEAR_OK;
+    Table* t = reinterpret_cast<Table*>(h);
+    gear::DeviceGuard guard(t->device);
+    hipError_t e = hipDeviceSynchronize();
+    free_table(t);
+    if (e != hipSuccess) return hip_fail(e, "gear_table_destroy: hipDeviceSynchronize");
+    return GEAR_OK;
+}
+
+extern "C" int gear_insert(gear_table* h, int64_t n, const void* const* col_src, const uint32_t* priorities,
+                           void* stream) {
+    if (h == nullptr) return fail(GEAR_E_INVAL, "gear_insert: table is NULL");
+    Table* t = reinterpret_cast<Table*>(h);
+    if (n < 0) return fail(GEAR_E_INVAL, "gear_insert: n < 0");
+    if (n == 0) return GEAR_OK;
+    if (priorities == nullptr) return fail(GEAR_E_INVAL, "gear_insert: priorities is NULL");
+    if (t->ncols > 0) {
+        if (col_src == nullptr) return fail(GEAR_E_INVAL, "gear_insert: col_src is NULL");
+        for (int c = 0; c < t->ncols; c++)
+            if (col_src[c] == nullptr) return fail(GEAR_E_INVAL, "gear_insert: a column source is NULL");
+    }
+    gear::DeviceGuard guard(t->device);
+    if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_insert: hipSetDevice");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    // Rows written one after another into slot k mod N: only the last N
+    // of a longer batch survive, so copy those.
+    const int64_t skip = n > t->N ? n - t->N : 0;
+    const int64_t rows = n - skip;
+    const int64_t slot0 = (int64_t)((t->next_seq + (uint64_t)skip) % (uint64_t)t->N);
+    const int64_t first = rows < t->N - slot0 ? rows : t->N - slot0;
+    const int64_t second = rows - first;
+
+    for (int c = 0; c < t->ncols; c++) {
+        const size_t rb = (size_t)t->T * (size_t)t->elem_bytes[c];
+        uint8_t* base = t->residency == GEAR_HOST_PINNED ? t->col_host[c] : t->col_dev[c];
+        const uint8_t* src = static_cast<const uint8_t*>(col_src[c]) + (size_t)skip * rb;
+        hipError_t e = hipMemcpyAsync(base + (size_t)slot0 * rb, src, (size_t)first * rb, hipMemcpyDefault, s);
+        if (e == hipSuccess && second > 0)
+            e = hipMemcpyAsync(base, src + (size_t)first * rb, (size_t)second * rb, hipMemcpyDefault, s);
+        if (e != hipSuccess) return hip_fail(e, "gear_insert: column copy");
+    }
+    const uint32_t* psrc = priorities + skip;
+    hipError_t e = hipMemcpyAsync(t->priority + slot0, psrc, sizeof(uint32_t) * first, hipMemcpyDefault, s);
+    if (e == hipSuccess && second > 0)
+        e = hipMemcpyAsync(t->priority, psrc + first, sizeof(uint32_t) * second, hipMemcpyDefault, s);
+    if (e != hipSuccess) return hip_fail(e, "gear_insert: priority copy");
+    t->next_seq += (uint64_t)n;
+    t->cdf_dirty = true;
+    return GEAR_OK;
+}
+
+extern "C" int gear_table_sync(gear_table* h, void* stream, int32_t* device_status) {
+    if (h == nullptr) return fail(GEAR_E_INVAL, "gear_table_sync: table is NULL");
+    Table* t = reinterpret_cast<Table*>(h);
+    gear::DeviceGuard guard(t->device);
+    if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_table_sync: hipSetDevice");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint32_t st = 0;
+    hipError_t e = hipMemcpyAsync(&st, t->status, sizeof(uint32_t), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemsetAsync(t->status, 0, sizeof(uint32_t), s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "gear_table_sync");
+    if (device_status) *device_status = (int32_t)st;
+    return GEAR_OK;
+}
+
+extern "C" int gear_table_info(const gear_table* h, int64_t* count, uint64_t* next_seq) {
+    if (h == nullptr) return fail(GEAR_E_INVAL, "gear_table_info: table is NULL");
+    const Table* t = reinterpret_cast<const Table*>(h);
+    if (count) *count = t->next_seq < (uint64_t)t->N ? (int64_t)t->next_seq : t->N;
+    if (next_seq) *next_seq = t->next_seq;
+    return GEAR_OK;
+}
+
+extern "C" int gear_table_column(const gear_table* h, int32_t c, void** base, void** host_ptr,
+                                 int64_t* elem_bytes) {
+    if (h == nullptr) return fail(GEAR_E_INVAL, "gear_table_column: table is NULL");
+    const Table* t = reinterpret_cast<const Table*>(h);
+    if (c < 0 || c >= t->ncols) return fail(GEAR_E_INVAL, "gear_table_column: no such column");
+    if (base) *base = t->col_dev[c];
+    if (host_ptr) *host_ptr = t->col_host[c];
+    if (elem_bytes) *elem_bytes = t->elem_bytes[c];
+    return GEAR_OK;
+}
+
+extern "C" int gear_table_priorities(const gear_table* h, uint32_t** d_priority) {
+    if (h == nullptr || d_priority == nullptr) return fail(GEAR_E_INVAL, "gear_table_priorities: NULL argument");
+    *d_priority = reinterpret_cast<const Table*>(h)->priority;
+    return GEAR_OK;
+}
+
+extern "C" const char* gear_last_error(void) {
+    return gear::g_last_error.c_str();
+}

@@ -1,0 +1,250 @@
+"""Python binding of libgear.so (the C ABI declared in include/gear.h).
+
+Each ``gear_*`` function here has the name and meaning of the C entry point
+and only marshals arguments: pointers are Python ints (a torch tensor's
+``data_ptr()``), streams are ``hipStream_t`` handles as ints (torch's
+``cuda_stream``; 0 is the null stream).  Every step of the hot path runs in
+the HIP library; a failing call raises ``GearError``.  ``Table`` is a
+convenience wrapper that takes torch tensors and uses torch only to allocate
+device memory and to name the current stream.
+"""
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libgear.so")
+
+GEAR_OK = 0
+GEAR_E_INVAL = -1
+GEAR_E_NOMEM = -2
+GEAR_E_EMPTY = -3
+GEAR_E_INSUFFICIENT = -4
+GEAR_E_HIP = -5
+GEAR_STATUS_NO_WEIGHT = 1
+GEAR_STATUS_BAD_INDEX = 2
+GEAR_STATUS_INTERNAL = 4
+GEAR_DEVICE = 0
+GEAR_HOST_PINNED = 1
+GEAR_FIFO = 0
+GEAR_LIFO = 1
+GEAR_UNIFORM = 2
+GEAR_PRIORITIZED = 3
+
+
+class GearError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__("%s (code %d)" % (msg, code))
+        self.code = code
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libgear.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libgear.so is not built at %s: run __graft_entry__.build() "
+                               "or python -m paper_2310_05205_amd.build" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, u64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
+        L.gear_table_create.argtypes = [vp, i32, i64, i32, i32, i32, ctypes.POINTER(vp)]
+        L.gear_table_destroy.argtypes = [vp]
+        L.gear_insert.argtypes = [vp, i64, vp, vp, vp]
+        L.gear_select.argtypes = [vp, i32, i32, i32, u64, ctypes.c_float, vp, vp, vp, vp]
+        L.gear_collect.argtypes = [vp, vp, vp, i32, i32, vp, i32, vp, vp]
+        L.gear_update_priorities.argtypes = [vp, vp, vp, i32, vp]
+        L.gear_table_sync.argtypes = [vp, vp, ctypes.POINTER(i32)]
+        L.gear_table_info.argtypes = [vp, ctypes.POINTER(i64), ctypes.POINTER(u64)]
+        L.gear_table_column.argtypes = [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(i64)]
+        L.gear_table_priorities.argtypes = [vp, ctypes.POINTER(vp)]
+        for name in ["gear_table_create", "gear_table_destroy", "gear_insert", "gear_select", "gear_collect",
+                     "gear_update_priorities", "gear_table_sync", "gear_table_info", "gear_table_column",
+                     "gear_table_priorities"]:
+            getattr(L, name).restype = ctypes.c_int
+        L.gear_last_error.argtypes = []
+        L.gear_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def gear_last_error():
+    return lib().gear_last_error().decode()
+
+
+def _check(code):
+    if code != GEAR_OK:
+        raise GearError(code, gear_last_error())
+    return code
+
+
+def _ptr_array(ptrs):
+    arr = (ctypes.c_void_p * max(len(ptrs), 1))()
+    for i, p in enumerate(ptrs):
+        arr[i] = p
+    return arr
+
+
+def gear_table_create(elem_bytes, capacity, T, residency=GEAR_DEVICE, device=0):
+    eb = (ctypes.c_int64 * max(len(elem_bytes), 1))(*[int(e) for e in elem_bytes])
+    out = ctypes.c_void_p()
+    _check(lib().gear_table_create(eb, len(elem_bytes), int(capacity), int(T), int(residency), int(device),
+                                   ctypes.byref(out)))
+    return out.value
+
+
+def gear_table_destroy(table):
+    _check(lib().gear_table_destroy(table))
+
+
+def gear_insert(table, n, col_src, priorities, stream=0):
+    """col_src: list of pointers (host or device), priorities: pointer."""
+    arr = _ptr_array(col_src) if col_src is not None else None
+    _check(lib().gear_insert(table, int(n), arr, priorities, stream))
+
+
+def gear_select(table, strategy, B, L, seed, beta, d_idx, d_start, d_weights=0, stream=0):
+    _check(lib().gear_select(table, int(strategy), int(B), int(L), int(seed) & ((1 << 64) - 1),
+                             ctypes.c_float(beta), d_idx, d_start, d_weights or None, stream))
+
+
+def gear_collect(table, d_idx, d_start, B, L, col_ids, d_out, stream=0):
+    """col_ids: list of column numbers or None (all); d_out: list of device pointers."""
+    ids = (ctypes.c_int32 * len(col_ids))(*col_ids) if col_ids is not None else None
+    _check(lib().gear_collect(table, d_idx, d_start, int(B), int(L), ids, len(d_out), _ptr_array(d_out), stream))
+
+
+def gear_update_priorities(table, d_idx, d_new_priorities, B, stream=0):
+    _check(lib().gear_update_priorities(table, d_idx, d_new_priorities, int(B), stream))
+
+
+def gear_table_sync(table, stream=0):
+    st = ctypes.c_int32(0)
+    _check(lib().gear_table_sync(table, stream, ctypes.byref(st)))
+    return st.value
+
+
+def gear_table_info(table):
+    count = ctypes.c_int64(0)
+    nseq = ctypes.c_uint64(0)
+    _check(lib().gear_table_info(table, ctypes.byref(count), ctypes.byref(nseq)))
+    return count.value, nseq.value
+
+
+def gear_table_column(table, c):
+    base = ctypes.c_void_p()
+    host = ctypes.c_void_p()
+    eb = ctypes.c_int64(0)
+    _check(lib().gear_table_column(table, int(c), ctypes.byref(base), ctypes.byref(host), ctypes.byref(eb)))
+    return base.value, host.value, eb.value
+
+
+def gear_table_priorities(table):
+    p = ctypes.c_void_p()
+    _check(lib().gear_table_priorities(table, ctypes.byref(p)))
+    return p.value
+
+
+class Table:
+    """A replay store over torch tensors.
+
+    ``columns`` is a list of bytes-per-step sizes.  Outputs are allocated as
+    torch CUDA tensors on the table's device; work is issued on torch's
+    current stream of that device.
+    """
+
+    def __init__(self, elem_bytes, capacity, T, residency=GEAR_DEVICE, device=0):
+        import torch
+        self._torch = torch
+        self.elem_bytes = [int(e) for e in elem_bytes]
+        self.capacity, self.T, self.device = int(capacity), int(T), int(device)
+        self.residency = residency
+        self.handle = gear_table_create(self.elem_bytes, capacity, T, residency, device)
+
+    def close(self):
+        if self.handle:
+            gear_table_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _stream(self, stream):
+        if stream is not None:
+            return stream.cuda_stream
+        return self._torch.cuda.current_stream(self.device).cuda_stream
+
+    def insert(self, col_src, priorities, stream=None):
+        """col_src: list of tensors/arrays [n, T*E_c] bytes (host or device); priorities uint32[n]."""
+        n = int(priorities.shape[0])
+        ptrs = [_data_ptr(x) for x in col_src]
+        gear_insert(self.handle, n, ptrs, _data_ptr(priorities), self._stream(stream))
+
+    def select(self, strategy, B, L, seed, beta=0.0, weights=False, stream=None):
+        torch = self._torch
+        dev = torch.device("cuda", self.device)
+        idx = torch.empty(B, dtype=torch.int64, device=dev)
+        start = torch.empty(B, dtype=torch.int32, device=dev)
+        w = torch.empty(B, dtype=torch.float32, device=dev) if weights else None
+        gear_select(self.handle, strategy, B, L, seed, beta, idx.data_ptr(), start.data_ptr(),
+                    w.data_ptr() if w is not None else 0, self._stream(stream))
+        return idx, start, w
+
+    def collect(self, idx, start, L, col_ids=None, stream=None, out=None):
+        """Returns a list of uint8 tensors [B, L*E_c], one per requested column."""
+        torch = self._torch
+        B = int(idx.shape[0])
+        cols = list(range(len(self.elem_bytes))) if col_ids is None else list(col_ids)
+        if out is None:
+            dev = torch.device("cuda", self.device)
+            out = [torch.empty((B, L * self.elem_bytes[c]), dtype=torch.uint8, device=dev) for c in cols]
+        gear_collect(self.handle, idx.data_ptr(), start.data_ptr(), B, L, col_ids,
+                     [o.data_ptr() for o in out], self._stream(stream))
+        return out
+
+    def update_priorities(self, idx, new_priorities, stream=None):
+        gear_update_priorities(self.handle, idx.data_ptr(), new_priorities.data_ptr(), int(idx.shape[0]),
+                               self._stream(stream))
+
+    def sync(self, stream=None):
+        return gear_table_sync(self.handle, self._stream(stream))
+
+    def info(self):
+        return gear_table_info(self.handle)
+
+    def priorities(self):
+        """Copy of the priority array as a CPU uint32 numpy array."""
+        import numpy as np
+        torch = self._torch
+        ptr = gear_table_priorities(self.handle)
+        host = np.empty(self.capacity, dtype=np.uint32)
+        torch.cuda.synchronize(self.device)
+        _hip_memcpy_d2h(host.ctypes.data, ptr, host.nbytes)
+        return host
+
+
+def _data_ptr(x):
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    return x.ctypes.data
+
+
+_hip = None
+
+
+def _hip_memcpy_d2h(dst, src, nbytes):
+    """Plain hipMemcpy for reading table state back (tests, checks)."""
+    global _hip
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so")
+        _hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+        _hip.hipMemcpy.restype = ctypes.c_int
+    rc = _hip.hipMemcpy(dst, src, nbytes, 2)  # hipMemcpyDeviceToHost
+    if rc != 0:
+        raise RuntimeError("hipMemcpy failed (%d)" % rc)

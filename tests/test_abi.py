@@ -1,0 +1,71 @@
+"""CPU checks of the C ABI: the library loads, exports every function that
+include/gear.h declares, and rejects invalid arguments before touching a
+device.  No compute call is made here."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2310_05205_amd import gear
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "gear.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gear_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert "gear_select" in names and "gear_collect" in names and len(names) >= 10
+    lib = gear.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_header_constants_match_binding():
+    with open(os.path.join(ROOT, "include", "gear.h")) as f:
+        text = f.read()
+    for name, val in re.findall(r"#define (GEAR_[A-Z_]+)\s+(-?\d+)u?\b", text):
+        if hasattr(gear, name):
+            assert getattr(gear, name) == int(val), name
+
+
+def test_argument_validation_without_device():
+    lib = gear.lib()
+    out = ctypes.c_void_p()
+    eb = (ctypes.c_int64 * 1)(4)
+    assert lib.gear_table_create(eb, 1, 16, 4, 0, 0, None) == gear.GEAR_E_INVAL
+    assert lib.gear_table_create(eb, 1, 0, 4, 0, 0, ctypes.byref(out)) == gear.GEAR_E_INVAL
+    assert lib.gear_table_create(eb, 1, 16, 0, 0, 0, ctypes.byref(out)) == gear.GEAR_E_INVAL
+    assert lib.gear_table_create(eb, 1, 16, 4, 7, 0, ctypes.byref(out)) == gear.GEAR_E_INVAL
+    assert lib.gear_table_create(eb, -1, 16, 4, 0, 0, ctypes.byref(out)) == gear.GEAR_E_INVAL
+    assert lib.gear_table_create(None, 1, 16, 4, 0, 0, ctypes.byref(out)) == gear.GEAR_E_INVAL
+    assert lib.gear_table_create(eb, 1, (1 << 30) + 1, 4, 0, 0, ctypes.byref(out)) == gear.GEAR_E_INVAL
+    assert "capacity" in gear.gear_last_error()
+    assert lib.gear_select(None, 3, 1, 1, 0, ctypes.c_float(0), None, None, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_collect(None, None, None, 1, 1, None, 1, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_update_priorities(None, None, None, 1, None) == gear.GEAR_E_INVAL
+    assert lib.gear_insert(None, 1, None, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_table_sync(None, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_table_info(None, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_table_destroy(None) == gear.GEAR_OK
+    with pytest.raises(gear.GearError) as e:
+        gear.gear_table_create([4], 16, 0)
+    assert e.value.code == gear.GEAR_E_INVAL
+
+
+def test_product_has_no_oracle_or_fallback():
+    """The product package must not reach the oracle or a CPU path."""
+    pkg = os.path.join(ROOT, "paper_2310_05205_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".h", ".cpp")):
+                with open(os.path.join(dirpath, fn)) as f:
+                    src = f.read()
+                assert "import oracle" not in src and "from oracle" not in src, fn
+                assert "oracle_" not in src, fn
