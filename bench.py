@@ -1,0 +1,254 @@
+#!/usr/bin/env python3
+"""Benchmark of the replay hot path on one MI355X.
+
+One step = prioritized selection (prefix scan, B draws, importance-sampling
+weights) + collection of the B selected L-step windows of every column +
+priority-update scatter, on a synthetic table resident in HBM (default
+workload: MAT-shaped, N=500000 trajectories x T=200 steps, B=8192, L=32).
+Inputs are generated and inserted before the timed region.
+
+Prints one JSON line.  `value` is trajectory-steps gathered per second over
+the whole step; `roofline` rates the gather kernel (the dominant kernel)
+against its bandwidth peak from HIP events around each gather launch in the
+timed region; `cpu_baseline` is the plain CPU oracle timed on a bounded
+sample of the same workload.
+
+  python bench.py [--steps K] [--warmup W] [--workload mat|gato-host|dt|tiny|select-stress]
+  python bench.py --calibrate     # plain copy kernel of known size, for counter scaling
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "trajectory-steps gathered/sec + gather GB/s as % of HBM / host-link peak"
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
+HOST_LINK_PEAK_GBS = 63.0       # PCIe Gen5 x16 per direction: 32 GT/s * 16 * 128/130 / 8
+GATHER_SRC = os.path.join(ROOT, "paper_2310_05205_amd", "csrc", "collect.hip")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="mat", choices=["mat", "gato-host", "dt", "tiny", "select-stress"])
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target oracle time for the CPU baseline")
+    ap.add_argument("--calibrate", action="store_true", help="run a plain copy kernel of known size and exit")
+    return ap.parse_args()
+
+
+def workload(name):
+    from gen import configs
+    return {"mat": configs.MAT, "gato-host": configs.GATO_HOST, "dt": configs.DT, "tiny": configs.TINY,
+            "select-stress": configs.SELECT_STRESS}[name]
+
+
+def calibrate():
+    """A plain elementwise copy (bitwise_not of int64) of 2 GiB: reads and
+    writes exactly 2 GiB per launch, for scaling FETCH_SIZE/WRITE_SIZE."""
+    import torch
+    n = (2 << 30) // 8
+    a = torch.zeros(n, dtype=torch.int64, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(5):
+        torch.bitwise_not(a, out=b)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate": "bitwise_not int64", "bytes_read_per_launch": n * 8,
+                      "bytes_written_per_launch": n * 8, "launches": 5}))
+
+
+def source_sha(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def profiled_traffic(kernel_key, workload_name):
+    """HBM bytes per gather launch from the committed counter summary, if it
+    was taken on the current gather source; else None."""
+    path = os.path.join(ROOT, "profiles", "gather_%s_counters.txt" % workload_name)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("source_sha256") != source_sha(GATHER_SRC) or vals.get("kernel") != kernel_key:
+        return None
+    try:
+        return float(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, target_s):
+    """The oracle, single-threaded, on a bounded sample: repeated steps of
+    the same workload (select over all N priorities, IS weights, collection
+    of the B selected windows, update), collecting from a compact host table
+    that holds only the trajectories the first selection picks."""
+    import numpy as np
+
+    import gen
+    import oracle
+    from tests.helpers import oracle_priorities
+
+    p, next_seq = oracle_priorities(w)
+    seed = gen.select_seed(w.seed, 0)
+    st, idx, start, _ = oracle.select(oracle.PRIORITIZED, p, next_seq, w.T, w.B, w.L, seed, w.beta, True)
+    assert st == oracle.OK
+    ks = gen.slot_insertion(idx, next_seq, w.N)
+    rows = [gen.fill_rows_list_cpu(c, ci, w.seed, w.T, ks) for ci, c in enumerate(w.columns)]
+    local = np.arange(w.B, dtype=np.int64)
+    newp = gen.update_priorities(w.prio, w.seed, 0, w.B)
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        st, oidx, ostart, ow = oracle.select(oracle.PRIORITIZED, p, next_seq, w.T, w.B, w.L, seed, w.beta, True)
+        if rows:
+            st2, outs = oracle.collect(rows, w.T, local, ostart, w.L)
+            del outs
+        oracle.update(p, oidx, newp)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= target_s:
+            break
+    return {"value": w.B * w.L * reps / el, "unit": "trajectory-steps/s", "cores": 1, "kind": "oracle",
+            "sample": "%d repetitions of one step (select over all %d priorities with IS weights, collect of "
+                      "the %d selected %d-step windows from a compact host table of the selected "
+                      "trajectories, update) in %.1f s on one host core" % (reps, w.N, w.B, w.L, el)}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (requested %d GPUs, WORLD_SIZE=%d)"
+              % (args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+    if args.calibrate:
+        calibrate()
+        return
+
+    import numpy as np
+    import torch
+
+    import gen
+    from gen.fill import fill_table
+    from paper_2310_05205_amd import gear
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    gear.lib()  # fails loudly if the library is not built
+    w = workload(args.workload)
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+
+    host_table = w.host_table
+    t = gear.Table(w.elem_bytes, w.N, w.T, gear.GEAR_HOST_PINNED if host_table else gear.GEAR_DEVICE, 0)
+    fill_table(w, lambda n, ptrs, prio: t.insert(ptrs, prio), device=0)
+
+    K, W = args.steps, args.warmup
+    B, L = w.B, w.L
+    strategy = w.strategies[0]
+    prioritized = strategy == gear.GEAR_PRIORITIZED
+    idx = torch.empty(B, dtype=torch.int64, device=dev)
+    start = torch.empty(B, dtype=torch.int32, device=dev)
+    wts = torch.empty(B, dtype=torch.float32, device=dev)
+    outs = [torch.empty(B * L * e, dtype=torch.uint8, device=dev) for e in w.elem_bytes]
+    out_ptrs = [o.data_ptr() for o in outs]
+    newp = torch.from_numpy(np.stack([gen.update_priorities(w.prio, w.seed, it, B) for it in range(W + K)])).to(dev)
+    seeds = [gen.select_seed(w.seed, it) for it in range(W + K)]
+    batch_bytes = B * L * sum(w.elem_bytes)
+
+    def step(it):
+        gear.gear_select(t.handle, strategy, B, L, seeds[it], w.beta, idx.data_ptr(), start.data_ptr(),
+                         wts.data_ptr() if w.weights else 0, sh)
+        if outs:
+            gear.gear_collect(t.handle, idx.data_ptr(), start.data_ptr(), B, L, None, out_ptrs, sh)
+        if prioritized:
+            gear.gear_update_priorities(t.handle, idx.data_ptr(), newp[it].data_ptr(), B, sh)
+
+    for it in range(W):
+        step(it)
+    torch.cuda.synchronize()
+    if t.sync() != 0:
+        raise SystemExit("device status set during warm-up")
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        it = W + k
+        e = ev[k]
+        e[0].record(stream)
+        gear.gear_select(t.handle, strategy, B, L, seeds[it], w.beta, idx.data_ptr(), start.data_ptr(),
+                         wts.data_ptr() if w.weights else 0, sh)
+        e[1].record(stream)
+        if outs:
+            gear.gear_collect(t.handle, idx.data_ptr(), start.data_ptr(), B, L, None, out_ptrs, sh)
+        e[2].record(stream)
+        if prioritized:
+            gear.gear_update_priorities(t.handle, idx.data_ptr(), newp[it].data_ptr(), B, sh)
+        e[3].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    status = t.sync()
+    if status != 0:
+        raise SystemExit("device status %d set during the timed steps" % status)
+
+    wall = t1 - t0
+    sel_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    col_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    upd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
+
+    if host_table:
+        alg_bytes = batch_bytes                  # bytes crossing the host link
+        peak, bound = HOST_LINK_PEAK_GBS, "host-link"
+    else:
+        alg_bytes = 2 * batch_bytes              # window bytes read + batch bytes written
+        peak, bound = HBM_PEAK_GBS, "hbm"
+    roof = None
+    if outs:
+        achieved = alg_bytes / (col_ms * 1e-3) / 1e9
+        roof = {"bound": bound, "achieved": round(achieved, 1), "peak": peak, "unit": "GB/s",
+                "frac": round(achieved / peak, 4),
+                "traffic": profiled_traffic("collect_kernel", args.workload),
+                "kernel": "collect_kernel", "algorithmic_bytes_per_launch": alg_bytes,
+                "avg_launch_ms": round(col_ms, 5)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, args.cpu_seconds)
+
+    steps_per_s = B * L * K / wall
+    line = {
+        "metric": METRIC, "value": round(steps_per_s, 1), "unit": "trajectory-steps/s", "n_gpus": 1,
+        "steps": K, "warmup": W, "ms_per_step": round(wall * 1e3 / K, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+        "config": {"workload": w.name, "N": w.N, "T": w.T, "B": B, "L": L,
+                   "columns": {c.name: "%s[%d]" % (c.dtype, c.m) for c in w.columns},
+                   "elem_bytes": w.elem_bytes, "table_bytes": w.table_bytes,
+                   "residency": "pinned-host" if host_table else "hbm",
+                   "strategy": {0: "fifo", 1: "lifo", 2: "uniform", 3: "prioritized"}[strategy],
+                   "is_weights": bool(w.weights), "parallelism": "1 GPU"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "stages_ms": {"select": round(sel_ms, 5), "collect": round(col_ms, 5), "update": round(upd_ms, 5)},
+        "selection_samples_per_s": round(B / (sel_ms * 1e-3), 1),
+        "batch_bytes": batch_bytes,
+    }
+    t.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

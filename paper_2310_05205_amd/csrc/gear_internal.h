@@ -21,6 +21,9 @@ constexpr int kTilesPerChunk = 16;
 constexpr int kChunk = kTile * kTilesPerChunk;
 constexpr int kFanout = 256;
 constexpr int kMaxLevels = 6;
+// The search runs at most this many workgroups; each leaves the smallest
+// priority its draws selected in one slot of Table::wg_min.
+constexpr int kSearchMaxGrid = 2048;
 
 struct Table {
     int device = 0;
@@ -44,11 +47,10 @@ struct Table {
     uint64_t* level[kMaxLevels] = {};
     uint64_t* lookback = nullptr;     // [2][nchunks] packed (state, value) words
     uint32_t* ticket = nullptr;       // [2] chunk tickets, double-buffered
-    unsigned long long* pmin = nullptr;  // batch minimum priority, epoch-tagged
+    uint32_t* wg_min = nullptr;       // [kSearchMaxGrid] per-workgroup minimum selected priority
     uint32_t* status = nullptr;       // device status word
     int scan_parity = 0;
     bool cdf_dirty = true;
-    uint32_t select_epoch = 0;
 };
 
 // Thread-local error reporting.
@@ -70,9 +72,9 @@ class DeviceGuard {
 // Kernel launchers (each returns hipSuccess or the launch error).
 hipError_t launch_scan(Table& t, hipStream_t s);
 hipError_t launch_search(Table& t, int32_t B, int32_t L, uint64_t seed, bool want_min,
-                         int64_t* idx, int32_t* start, hipStream_t s);
-hipError_t launch_is_weights(Table& t, int32_t B, float beta, const int64_t* idx, float* w,
-                             hipStream_t s);
+                         int64_t* idx, int32_t* start, int* grid_out, hipStream_t s);
+hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, const int64_t* idx,
+                             float* w, hipStream_t s);
 hipError_t launch_simple_select(Table& t, int32_t strategy, int32_t B, int32_t L, uint64_t seed,
                                 int64_t* idx, int32_t* start, float* w, hipStream_t s);
 hipError_t launch_scatter(Table& t, const int64_t* idx, const uint32_t* newp, int32_t B,

@@ -198,14 +198,15 @@ __device__ inline int64_t descend_level(const uint64_t* __restrict__ a, int64_t 
 
 __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict__ prio, int64_t N, Levels lv,
                                                      int32_t B, uint64_t span, uint64_t seed, int want_min,
-                                                     unsigned long long* pmin, uint32_t min_tag,
-                                                     uint32_t* status, int64_t* __restrict__ idx,
-                                                     int32_t* __restrict__ start) {
+                                                     uint32_t* __restrict__ wg_min, uint32_t* status,
+                                                     int64_t* __restrict__ idx, int32_t* __restrict__ start) {
+    __shared__ uint32_t s_min[4];
     const int lane = threadIdx.x & 63;
     const int64_t wave_id = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
     const int top = lv.nlevels - 1;
     const uint64_t S = lv.level[top][lv.size[top] - 1];
+    uint32_t my_min = 0xFFFFFFFFu;  // smallest priority this wave selected
 
     for (int64_t b = wave_id; b < B; b += nwaves) {
         if (S == 0) {
@@ -244,27 +245,50 @@ __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict_
             start[b] = (int32_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b + 1), span);
         }
         if (want_min) {
-            const uint64_t pv = __shfl((uint64_t)pick4(p0, p1, p2, p3, cnt & 3), cnt >> 2);
-            if (lane == 0) atomicMin(pmin, ((unsigned long long)min_tag << 32) | pv);
+            const uint32_t pv = (uint32_t)__shfl((uint64_t)pick4(p0, p1, p2, p3, cnt & 3), cnt >> 2);
+            my_min = pv < my_min ? pv : my_min;
+        }
+    }
+    if (want_min) {
+        // One slot per workgroup, no atomics: the weight kernel reduces them.
+        if (lane == 0) s_min[threadIdx.x >> 6] = my_min;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint32_t m = s_min[0];
+            for (int k = 1; k < (int)(blockDim.x >> 6); k++) m = s_min[k] < m ? s_min[k] : m;
+            wg_min[blockIdx.x] = m;
         }
     }
 }
 
 // w_b = (n*P(i_b))^-beta / max_b' (n*P(i_b'))^-beta = (p_min / p_b)^beta,
-// p_min the smallest selected priority; fp64, rounded once to fp32.
-__global__ void is_weights_kernel(const uint32_t* __restrict__ prio, int64_t N, const int64_t* __restrict__ idx, int32_t B,
-                                  double beta, const unsigned long long* pmin, uint32_t min_tag,
-                                  float* __restrict__ w) {
+// p_min the smallest selected priority; fp64, rounded once to fp32.  Every
+// workgroup first reduces the search's per-workgroup minima.
+__global__ __launch_bounds__(256) void is_weights_kernel(const uint32_t* __restrict__ prio, int64_t N,
+                                                         const int64_t* __restrict__ idx, int32_t B, double beta,
+                                                         const uint32_t* __restrict__ wg_min, int search_grid,
+                                                         float* __restrict__ w) {
+    __shared__ uint32_t s_min[4];
+    uint32_t m = 0xFFFFFFFFu;
+    for (int k = threadIdx.x; k < search_grid; k += blockDim.x) m = wg_min[k] < m ? wg_min[k] : m;
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+        const uint32_t o = __shfl_xor(m, d);
+        m = o < m ? o : m;
+    }
+    if ((threadIdx.x & 63) == 0) s_min[threadIdx.x >> 6] = m;
+    __syncthreads();
+    m = s_min[0];
+    for (int k = 1; k < (int)(blockDim.x >> 6); k++) m = s_min[k] < m ? s_min[k] : m;
+
     const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= B) return;
-    const unsigned long long m = *pmin;
     const int64_t i = idx[b];
-    if (i < 0 || i >= N || (uint32_t)(m >> 32) != min_tag) {
+    if (i < 0 || i >= N || m == 0u) {
         w[b] = 0.0f;
         return;
     }
-    const double pm = (double)(uint32_t)m;
-    w[b] = (float)pow(pm / (double)prio[i], beta);
+    w[b] = (float)pow((double)m / (double)prio[i], beta);
 }
 
 // FIFO / LIFO: ring arithmetic from the oldest / newest live slot.
@@ -313,17 +337,19 @@ hipError_t launch_scan(Table& t, hipStream_t s) {
 }
 
 hipError_t launch_search(Table& t, int32_t B, int32_t L, uint64_t seed, bool want_min, int64_t* idx,
-                         int32_t* start, hipStream_t s) {
-    const unsigned grid = (unsigned)((B + 3) / 4);
+                         int32_t* start, int* grid_out, hipStream_t s) {
+    int64_t g = ((int64_t)B + 3) / 4;  // one wave per draw while the grid allows
+    const int grid = (int)(g < kSearchMaxGrid ? g : kSearchMaxGrid);
     hipLaunchKernelGGL(search_kernel, dim3(grid), dim3(256), 0, s, t.priority, t.N, make_levels(t), B,
-                       (uint64_t)(t.T - L + 1), seed, want_min ? 1 : 0, t.pmin, ~t.select_epoch, t.status, idx,
-                       start);
+                       (uint64_t)(t.T - L + 1), seed, want_min ? 1 : 0, t.wg_min, t.status, idx, start);
+    *grid_out = grid;
     return hipGetLastError();
 }
 
-hipError_t launch_is_weights(Table& t, int32_t B, float beta, const int64_t* idx, float* w, hipStream_t s) {
-    hipLaunchKernelGGL(is_weights_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s, t.priority, t.N, idx, B,
-                       (double)beta, t.pmin, ~t.select_epoch, w);
+hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, const int64_t* idx, float* w,
+                             hipStream_t s) {
+    hipLaunchKernelGGL(is_weights_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s, t.priority, t.N, idx,
+                       B, (double)beta, t.wg_min, search_grid, w);
     return hipGetLastError();
 }
 
@@ -369,19 +395,11 @@ extern "C" int gear_select(gear_table* h, int32_t strategy, int32_t B, int32_t L
         t->cdf_dirty = false;
     }
     const bool weights = d_weights != nullptr;
-    if (weights) {
-        // A new tag per weighted select makes the batch minimum restart
-        // without clearing it: newer tags compare smaller.
-        t->select_epoch++;
-        if (t->select_epoch == 0) {
-            hipError_t e = hipMemsetAsync(t->pmin, 0xFF, sizeof(unsigned long long), s);
-            if (e != hipSuccess) return hip_fail(e, "gear_select: resetting the batch minimum");
-        }
-    }
-    hipError_t e = gear::launch_search(*t, B, L, seed, weights, d_idx, d_start, s);
+    int grid = 0;
+    hipError_t e = gear::launch_search(*t, B, L, seed, weights, d_idx, d_start, &grid, s);
     if (e != hipSuccess) return hip_fail(e, "gear_select: search launch");
     if (weights) {
-        e = gear::launch_is_weights(*t, B, beta, d_idx, d_weights, s);
+        e = gear::launch_is_weights(*t, B, beta, grid, d_idx, d_weights, s);
         if (e != hipSuccess) return hip_fail(e, "gear_select: weight launch");
     }
     return GEAR_OK;

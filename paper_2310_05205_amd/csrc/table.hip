@@ -60,7 +60,7 @@ void free_table(Table* t) {
     for (int l = 0; l < gear::kMaxLevels; l++) (void)hipFree(t->level[l]);
     (void)hipFree(t->lookback);
     (void)hipFree(t->ticket);
-    (void)hipFree(t->pmin);
+    (void)hipFree(t->wg_min);
     (void)hipFree(t->status);
     delete t;
 }
@@ -161,14 +161,14 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
         if ((e = dmalloc(&t->level[l], sizeof(uint64_t) * t->level_size[l])) != hipSuccess) return oom("prefix levels", e);
     if ((e = dmalloc(&t->lookback, sizeof(uint64_t) * 2 * t->nchunks)) != hipSuccess) return oom("look-back words", e);
     if ((e = dmalloc(&t->ticket, sizeof(uint32_t) * 2)) != hipSuccess) return oom("tickets", e);
-    if ((e = dmalloc(&t->pmin, sizeof(unsigned long long))) != hipSuccess) return oom("batch minimum", e);
+    if ((e = dmalloc(&t->wg_min, sizeof(uint32_t) * gear::kSearchMaxGrid)) != hipSuccess) return oom("batch minima", e);
     if ((e = dmalloc(&t->status, sizeof(uint32_t))) != hipSuccess) return oom("status word", e);
 
     if ((e = hipMemset(t->priority, 0, sizeof(uint32_t) * capacity)) != hipSuccess ||
         (e = hipMemset(t->tag, 0, sizeof(uint32_t) * capacity)) != hipSuccess ||
         (e = hipMemset(t->lookback, 0, sizeof(uint64_t) * 2 * t->nchunks)) != hipSuccess ||
         (e = hipMemset(t->ticket, 0, sizeof(uint32_t) * 2)) != hipSuccess ||
-        (e = hipMemset(t->pmin, 0xFF, sizeof(unsigned long long))) != hipSuccess ||
+        (e = hipMemset(t->wg_min, 0xFF, sizeof(uint32_t) * gear::kSearchMaxGrid)) != hipSuccess ||
         (e = hipMemset(t->status, 0, sizeof(uint32_t))) != hipSuccess ||
         (e = hipDeviceSynchronize()) != hipSuccess) {
         free_table(t);
