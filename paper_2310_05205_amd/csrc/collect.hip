@@ -67,10 +67,18 @@ struct Elem<1> {
     typedef uint8_t type;
 };
 
-// Streaming loads: table bytes are read once per collection.
+// Table bytes are read once per collection: the loads are non-temporal.
+// The batch is stored normally (measured on gfx950 with fresh windows every
+// launch: non-temporal loads with plain stores beat plain loads, and beat
+// non-temporal stores).
 template <int WIDTH>
 __device__ inline typename Elem<WIDTH>::type load_stream(const typename Elem<WIDTH>::type* p) {
     return __builtin_nontemporal_load(p);
+}
+
+template <int WIDTH>
+__device__ inline void store_stream(typename Elem<WIDTH>::type* p, typename Elem<WIDTH>::type v) {
+    *p = v;
 }
 
 template <int WIDTH>
@@ -96,7 +104,7 @@ __device__ void copy_wide(const CollectArgs& a, const ColTask& c, int64_t q) {
     V* dst = reinterpret_cast<V*>(c.out + b * c.W + off0);
     const int64_t so = window_offset(a, c, b);
     if (so < 0) {
-        for (int64_t e = threadIdx.x; e < n; e += kThreads) dst[e] = zero_elem<WIDTH>();
+        for (int64_t e = threadIdx.x; e < n; e += kThreads) store_stream<WIDTH>(dst + e, zero_elem<WIDTH>());
         if (threadIdx.x == 0) atomicOr(a.status, GEAR_STATUS_BAD_INDEX);
         return;
     }
@@ -106,9 +114,9 @@ __device__ void copy_wide(const CollectArgs& a, const ColTask& c, int64_t q) {
 #pragma unroll
         for (int k = 0; k < kUnroll; k++) v[k] = load_stream<WIDTH>(src + threadIdx.x + k * kThreads);
 #pragma unroll
-        for (int k = 0; k < kUnroll; k++) dst[threadIdx.x + k * kThreads] = v[k];
+        for (int k = 0; k < kUnroll; k++) store_stream<WIDTH>(dst + threadIdx.x + k * kThreads, v[k]);
     } else {
-        for (int64_t e = threadIdx.x; e < n; e += kThreads) dst[e] = load_stream<WIDTH>(src + e);
+        for (int64_t e = threadIdx.x; e < n; e += kThreads) store_stream<WIDTH>(dst + e, load_stream<WIDTH>(src + e));
     }
 }
 
@@ -145,7 +153,7 @@ __device__ void copy_narrow(const CollectArgs& a, const ColTask& c, int64_t q) {
 #pragma unroll
     for (int k = 0; k < kUnroll; k++) {
         const uint32_t e = threadIdx.x + k * kThreads;
-        if (e < total) dst[e] = v[k];
+        if (e < total) store_stream<WIDTH>(dst + e, v[k]);
     }
 }
 

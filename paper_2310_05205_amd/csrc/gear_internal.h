@@ -13,12 +13,11 @@ namespace gear {
 
 // Priority scan geometry.  A tile is 256 priorities: one wave64, four per
 // lane, one 16-byte load per lane.  A chunk (one workgroup of the scan) is
-// 16 tiles.  The search descends a tree of inclusive prefix sums with fan-out
-// 256: level 0 holds the prefix at the end of every tile, level l the prefix
-// at the end of every 256^l tiles; the top level has at most 256 entries.
+// 32 tiles.  Selection walks a 256-ary sum tree: level 0 holds the sum of
+// every tile, level l the sum of every 256^l tiles; the top level has at most
+// 256 nodes.
 constexpr int kTile = 256;
-constexpr int kTilesPerChunk = 16;
-constexpr int kChunk = kTile * kTilesPerChunk;
+constexpr int kTilesPerChunk = 32;
 constexpr int kFanout = 256;
 constexpr int kMaxLevels = 6;
 // The search runs at most this many workgroups; each leaves the smallest
@@ -42,14 +41,14 @@ struct Table {
 
     // Scan / search state.
     int64_t ntiles = 0, nchunks = 0;
-    int nlevels = 0;                  // levels of the prefix tree (level 0 = per tile)
+    int nlevels = 0;                  // levels of the sum tree (level 0 = per tile)
     int64_t level_size[kMaxLevels] = {};
-    uint64_t* level[kMaxLevels] = {};
-    uint64_t* lookback = nullptr;     // [2][nchunks] packed (state, value) words
-    uint32_t* ticket = nullptr;       // [2] chunk tickets, double-buffered
+    uint64_t* tile_sums = nullptr;    // level 0, rewritten by every scan
+    uint64_t* upper[2][kMaxLevels] = {};  // levels >= 1, two copies: a scan adds into
+                                      // one and zeroes the other for the next scan
+    int tree_parity = 0;              // copy filled by the last scan
     uint32_t* wg_min = nullptr;       // [kSearchMaxGrid] per-workgroup minimum selected priority
     uint32_t* status = nullptr;       // device status word
-    int scan_parity = 0;
     bool cdf_dirty = true;
 };
 
@@ -72,9 +71,8 @@ class DeviceGuard {
 // Kernel launchers (each returns hipSuccess or the launch error).
 hipError_t launch_scan(Table& t, hipStream_t s);
 hipError_t launch_search(Table& t, int32_t B, int32_t L, uint64_t seed, bool want_min,
-                         int64_t* idx, int32_t* start, int* grid_out, hipStream_t s);
-hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, const int64_t* idx,
-                             float* w, hipStream_t s);
+                         int64_t* idx, int32_t* start, uint32_t* sel_prio, int* grid_out, hipStream_t s);
+hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, float* w, hipStream_t s);
 hipError_t launch_simple_select(Table& t, int32_t strategy, int32_t B, int32_t L, uint64_t seed,
                                 int64_t* idx, int32_t* start, float* w, hipStream_t s);
 hipError_t launch_scatter(Table& t, const int64_t* idx, const uint32_t* newp, int32_t B,

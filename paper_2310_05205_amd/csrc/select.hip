@@ -2,23 +2,26 @@
 //
 // Prioritized (weighted) sampling is a prefix sum over the priorities
 // followed by one search per uniform draw (Sec. 3.3, centralized selection).
-// It runs as two kernels:
+// Here the prefix sum is split between two kernels so that no workgroup ever
+// waits on another:
 //
-//   scan_kernel    one pass over the priorities with decoupled look-back.
-//                  Each workgroup reduces a 4096-priority chunk (16 tiles of
-//                  256), publishes its aggregate, looks back over its
-//                  predecessors' published words 64 at a time for its
-//                  exclusive prefix, and writes the global inclusive prefix
-//                  at the end of each of its tiles (level 0 of the prefix
-//                  tree) plus every 256^l-th of those (level l).  Nothing of
-//                  size N is written.
-//   search_kernel  one wave per draw: r = floor(u*S/2^64) for a splitmix64
-//                  output u, then a 256-ary descent of the prefix tree (four
-//                  entries per lane, ballot + popcount finds the first entry
-//                  greater than r), then a wave scan of the chosen tile's 256
-//                  priorities in registers and a final ballot.  The result is
-//                  the smallest i with C_i > r, i.e. the binary-search answer
-//                  over the full inclusive prefix C.
+//   scan_kernel    one pass over the priorities.  A workgroup reduces a
+//                  chunk of 32 tiles of 256 priorities, writes each tile's
+//                  sum (level 0 of a 256-ary sum tree) and adds the chunk's
+//                  sum into the one node of every higher level that covers
+//                  it (at most 8 chunks share a level-1 node).  The top
+//                  level has at most 256 nodes.
+//   search_kernel  one wave per draw: the wave loads the top level (four
+//                  nodes per lane), forms its inclusive prefix with a wave
+//                  scan in registers (the total is S), draws r =
+//                  floor(u*S/2^64), then descends: at each level it scans
+//                  the 256 children of the chosen node in registers, counts
+//                  the children whose inclusive prefix is <= r (ballot +
+//                  popcount), takes the next one and subtracts the prefix
+//                  before it from r; at the leaves it does the same over the
+//                  chosen tile's 256 priorities.  The index found is the
+//                  smallest i with C_i > r for the inclusive prefix C over
+//                  all priorities: the binary-search answer.
 //
 // FIFO, LIFO and uniform selection are one thread per draw.
 #include "gear_internal.h"
@@ -26,13 +29,8 @@
 namespace gear {
 namespace {
 
-constexpr uint64_t kValueMask = (1ull << 62) - 1;
-constexpr uint64_t kAggregate = 1ull << 62;
-constexpr uint64_t kInclusive = 2ull << 62;
-constexpr uint32_t kMaxSpins = 1u << 22;
-
 struct Levels {
-    uint64_t* level[kMaxLevels];
+    uint64_t* level[kMaxLevels];   // level 0: tile sums; level l: sums of 256^l tiles
     int64_t size[kMaxLevels];
     int nlevels;
 };
@@ -49,163 +47,151 @@ __device__ inline uint64_t splitmix64_out(uint64_t seed, uint64_t c) {
 // floor(u * n / 2^64): the high word of the 128-bit product.
 __device__ inline uint64_t scale_draw(uint64_t u, uint64_t n) { return __umul64hi(u, n); }
 
-__device__ inline uint64_t wave_sum(uint64_t v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+// Wave-level scans with DPP (gfx9 data-parallel primitives, all 64 lanes
+// active): row shifts by 1, 2, 4, 8 scan each row of 16 lanes, then the
+// row broadcasts of lanes 15 and 31 carry row totals forward.  A lane whose
+// DPP source is outside its row receives 0.  64-bit values move as two
+// 32-bit halves.
+template <int CTRL, int ROW_MASK>
+__device__ inline uint64_t dpp_u64(uint64_t v) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, ROW_MASK, 0xf, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, ROW_MASK, 0xf, false);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ inline uint64_t wave_inclusive_scan(uint64_t v) {
+    v += dpp_u64<0x111, 0xf>(v);  // row_shr:1
+    v += dpp_u64<0x112, 0xf>(v);  // row_shr:2
+    v += dpp_u64<0x114, 0xf>(v);  // row_shr:4
+    v += dpp_u64<0x118, 0xf>(v);  // row_shr:8
+    v += dpp_u64<0x142, 0xa>(v);  // row_bcast:15 into rows 1 and 3
+    v += dpp_u64<0x143, 0xc>(v);  // row_bcast:31 into rows 2 and 3
     return v;
 }
 
-__device__ inline uint64_t wave_inclusive_scan(uint64_t v, int lane) {
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        uint64_t o = __shfl_up(v, d);
-        if (lane >= d) v += o;
-    }
-    return v;
+// Value of v in lane `src` (src is the same in every lane).
+__device__ inline uint64_t read_lane(uint64_t v, int src) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, src);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), src);
+    return ((uint64_t)hi << 32) | lo;
 }
+
+__device__ inline uint64_t wave_sum(uint64_t v) { return read_lane(wave_inclusive_scan(v), 63); }
 
 __device__ inline uint64_t pick4(uint64_t a, uint64_t b, uint64_t c, uint64_t d, int q) {
     return q == 0 ? a : (q == 1 ? b : (q == 2 ? c : d));
 }
 
-__device__ inline uint64_t load_lookback(const uint64_t* p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Inclusive prefix of 256 values held four per lane (lane l holds values
+// 4l..4l+3): c0..c3 receive the prefix at this lane's four positions.
+__device__ inline void wave_prefix4(uint64_t v0, uint64_t v1, uint64_t v2, uint64_t v3, uint64_t& c0,
+                                    uint64_t& c1, uint64_t& c2, uint64_t& c3) {
+    const uint64_t part = v0 + v1 + v2 + v3;
+    const uint64_t excl = wave_inclusive_scan(part) - part;
+    c0 = excl + v0;
+    c1 = c0 + v1;
+    c2 = c1 + v2;
+    c3 = c2 + v3;
 }
 
-__device__ inline void store_lookback(uint64_t* p, uint64_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Among 256 positions whose inclusive prefixes are c0..c3 (four per lane),
+// the number whose prefix is <= r, i.e. the position of the first prefix
+// greater than r; r is reduced by the prefix before that position.
+__device__ inline int pick_child(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3, uint64_t& r) {
+    const int cnt = __popcll(__ballot(c0 <= r)) + __popcll(__ballot(c1 <= r)) + __popcll(__ballot(c2 <= r)) +
+                    __popcll(__ballot(c3 <= r));
+    if (cnt > 0) {
+        const int k = cnt - 1;
+        r -= read_lane(pick4(c0, c1, c2, c3, k & 3), k >> 2);
+    }
+    return cnt;
 }
 
-__global__ __launch_bounds__(256) void scan_kernel(const uint32_t* __restrict__ prio, int64_t N, int64_t ntiles,
-                                                   Levels lv, uint64_t* __restrict__ look_cur,
-                                                   uint64_t* __restrict__ look_next, uint32_t* ticket_cur,
-                                                   uint32_t* ticket_next, int64_t nchunks, uint32_t* status) {
-    __shared__ uint64_t tile_sum[kTilesPerChunk];
-    __shared__ int64_t s_chunk;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-
-    // Chunks are numbered in the order workgroups start, so a workgroup only
-    // ever waits on chunks whose workgroups are already running.
-    if (threadIdx.x == 0)
-        s_chunk = (int64_t)__hip_atomic_fetch_add(ticket_cur, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __syncthreads();
-    const int64_t chunk = s_chunk;
-    if (chunk >= nchunks) return;  // only if a previous scan was interrupted
-    if (threadIdx.x == 0) {
-        // Prepare the other look-back buffer and ticket for the next scan.
-        look_next[chunk] = 0;
-        if (chunk == 0) *ticket_next = 0;
-    }
-
-    // Tile sums: wave w owns tiles 4w .. 4w+3 of the chunk, one 16-byte
-    // load per lane per tile.
-    uint32_t x[4][4];
-#pragma unroll
-    for (int q = 0; q < 4; q++) {
-        const int64_t e = (chunk * kTilesPerChunk + wave * 4 + q) * kTile + lane * 4;
-        if (e + 4 <= N) {
-            uint4 v = *reinterpret_cast<const uint4*>(prio + e);
-            x[q][0] = v.x; x[q][1] = v.y; x[q][2] = v.z; x[q][3] = v.w;
-        } else {
-#pragma unroll
-            for (int k = 0; k < 4; k++) x[q][k] = (e + k < N) ? prio[e + k] : 0u;
-        }
-    }
-#pragma unroll
-    for (int q = 0; q < 4; q++) {
-        uint64_t s = (uint64_t)x[q][0] + x[q][1] + x[q][2] + x[q][3];
-        s = wave_sum(s);
-        if (lane == 0) tile_sum[wave * 4 + q] = s;
-    }
-    __syncthreads();
-    if (wave != 0) return;
-
-    const uint64_t local = wave_inclusive_scan(lane < kTilesPerChunk ? tile_sum[lane] : 0, lane);
-    const uint64_t aggregate = __shfl(local, kTilesPerChunk - 1);
-    uint64_t prefix = 0;
-    if (chunk == 0) {
-        if (lane == 0) store_lookback(&look_cur[0], kInclusive | aggregate);
-    } else {
-        if (lane == 0) store_lookback(&look_cur[chunk], kAggregate | aggregate);
-        int64_t base = chunk - 1;  // predecessor examined by lane 0
-        uint32_t spins = 0;
-        while (true) {
-            const int64_t pos = base - lane;
-            const uint64_t w = pos >= 0 ? load_lookback(&look_cur[pos]) : kInclusive;
-            const uint64_t state = w >> 62;
-            const unsigned long long not_ready = __ballot(state == 0);
-            const unsigned long long inclusive = __ballot(state == 2);
-            const int first_incl = inclusive ? __ffsll((long long)inclusive) - 1 : 64;
-            const int first_wait = not_ready ? __ffsll((long long)not_ready) - 1 : 64;
-            if (first_wait < first_incl) {
-                // A chunk we need has not published yet.  Its workgroup is
-                // running (tickets are taken in start order), so the wait
-                // ends; the bound only guarantees every wave exits.
-                if (++spins > kMaxSpins) {
-                    if (lane == 0) atomicOr(status, GEAR_STATUS_INTERNAL);
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(1);
-                continue;
-            }
-            const int upto = first_incl < 64 ? first_incl : 63;
-            prefix += wave_sum(lane <= upto ? (w & kValueMask) : 0);
-            if (first_incl < 64) break;
-            base -= 64;
-        }
-        if (lane == 0) store_lookback(&look_cur[chunk], kInclusive | (prefix + aggregate));
-    }
-
-    if (lane < kTilesPerChunk) {
-        const int64_t gt = chunk * kTilesPerChunk + lane;
-        if (gt < ntiles) {
-            const uint64_t c = prefix + local;
-            lv.level[0][gt] = c;
-            int64_t span = kFanout;
-            for (int l = 1; l < lv.nlevels; l++) {
-                if (((gt + 1) % span) == 0 || gt == ntiles - 1) lv.level[l][gt / span] = c;
-                span *= kFanout;
-            }
-        }
-    }
-}
-
-// Number of entries <= r among a[s0 .. s0+256) (entries at or past n count as
-// +inf), and the value of the last such entry (unchanged `lo` if none).
-__device__ inline int64_t descend_level(const uint64_t* __restrict__ a, int64_t n, int64_t s0, uint64_t r,
-                                        int lane, uint64_t& lo) {
-    const int64_t e = s0 + lane * 4;
-    uint64_t v0, v1, v2, v3;
+__device__ inline void load4_u64(const uint64_t* __restrict__ a, int64_t n, int64_t e, uint64_t& v0, uint64_t& v1,
+                                 uint64_t& v2, uint64_t& v3) {
     if (e + 4 <= n) {
         const ulonglong2 p0 = *reinterpret_cast<const ulonglong2*>(a + e);
         const ulonglong2 p1 = *reinterpret_cast<const ulonglong2*>(a + e + 2);
         v0 = p0.x; v1 = p0.y; v2 = p1.x; v3 = p1.y;
     } else {
-        v0 = e + 0 < n ? a[e + 0] : ~0ull;
-        v1 = e + 1 < n ? a[e + 1] : ~0ull;
-        v2 = e + 2 < n ? a[e + 2] : ~0ull;
-        v3 = e + 3 < n ? a[e + 3] : ~0ull;
+        v0 = e + 0 < n ? a[e + 0] : 0;
+        v1 = e + 1 < n ? a[e + 1] : 0;
+        v2 = e + 2 < n ? a[e + 2] : 0;
+        v3 = e + 3 < n ? a[e + 3] : 0;
     }
-    const int cnt = __popcll(__ballot(v0 <= r)) + __popcll(__ballot(v1 <= r)) + __popcll(__ballot(v2 <= r)) +
-                    __popcll(__ballot(v3 <= r));
-    if (cnt > 0) {
-        const int k = cnt - 1;
-        lo = __shfl(pick4(v0, v1, v2, v3, k & 3), k >> 2);
+}
+
+__device__ inline void load4_u32(const uint32_t* __restrict__ a, int64_t n, int64_t e, uint32_t& p0, uint32_t& p1,
+                                 uint32_t& p2, uint32_t& p3) {
+    if (e + 4 <= n) {
+        const uint4 v = *reinterpret_cast<const uint4*>(a + e);
+        p0 = v.x; p1 = v.y; p2 = v.z; p3 = v.w;
+    } else {
+        p0 = e + 0 < n ? a[e + 0] : 0u;
+        p1 = e + 1 < n ? a[e + 1] : 0u;
+        p2 = e + 2 < n ? a[e + 2] : 0u;
+        p3 = e + 3 < n ? a[e + 3] : 0u;
     }
-    return s0 + cnt;
+}
+
+// `upper` holds the levels >= 1 this scan adds into; `clear` the other copy
+// of those levels, which this scan zeroes for the next one (each node is
+// zeroed by the chunk that starts it).
+__global__ __launch_bounds__(256) void scan_kernel(const uint32_t* __restrict__ prio, int64_t N, Levels upper,
+                                                   Levels clear, uint64_t* __restrict__ tile_sums, int64_t ntiles) {
+    __shared__ uint64_t tile_sum[kTilesPerChunk];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int64_t chunk = blockIdx.x;
+    constexpr int kTilesPerWave = kTilesPerChunk / 4;
+
+    // Wave w owns tiles 8w .. 8w+7 of the chunk: eight 16-byte loads per
+    // lane, all issued before any is used.
+    uint32_t x[kTilesPerWave][4];
+#pragma unroll
+    for (int q = 0; q < kTilesPerWave; q++)
+        load4_u32(prio, N, (chunk * kTilesPerChunk + wave * kTilesPerWave + q) * kTile + lane * 4, x[q][0], x[q][1],
+                  x[q][2], x[q][3]);
+#pragma unroll
+    for (int q = 0; q < kTilesPerWave; q++) {
+        const uint64_t s = wave_sum((uint64_t)x[q][0] + x[q][1] + x[q][2] + x[q][3]);
+        const int64_t gt = chunk * kTilesPerChunk + wave * kTilesPerWave + q;
+        if (lane == 0) {
+            tile_sum[wave * kTilesPerWave + q] = s;
+            if (gt < ntiles) tile_sums[gt] = s;
+        }
+    }
+    __syncthreads();
+    if (wave != 0) return;
+    const uint64_t chunk_sum = wave_sum(lane < kTilesPerChunk ? tile_sum[lane] : 0);
+    // Lane l - 1 handles level l (>= 1).
+    const int l = lane + 1;
+    if (l < upper.nlevels) {
+        int64_t tiles_per_node = kFanout;
+        for (int k = 1; k < l; k++) tiles_per_node *= kFanout;
+        const int64_t first_tile = chunk * kTilesPerChunk;
+        const int64_t node = first_tile / tiles_per_node;
+        if (chunk_sum != 0) atomicAdd(reinterpret_cast<unsigned long long*>(upper.level[l] + node), chunk_sum);
+        if (first_tile % tiles_per_node == 0) clear.level[l][node] = 0;
+    }
 }
 
 __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict__ prio, int64_t N, Levels lv,
                                                      int32_t B, uint64_t span, uint64_t seed, int want_min,
                                                      uint32_t* __restrict__ wg_min, uint32_t* status,
-                                                     int64_t* __restrict__ idx, int32_t* __restrict__ start) {
+                                                     int64_t* __restrict__ idx, int32_t* __restrict__ start,
+                                                     uint32_t* __restrict__ sel_prio) {
     __shared__ uint32_t s_min[4];
     const int lane = threadIdx.x & 63;
     const int64_t wave_id = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
     const int top = lv.nlevels - 1;
-    const uint64_t S = lv.level[top][lv.size[top] - 1];
+
+    // The top level is the same for every draw: its prefix and total once.
+    uint64_t t0, t1, t2, t3, tc0, tc1, tc2, tc3;
+    load4_u64(lv.level[top], lv.size[top], lane * 4, t0, t1, t2, t3);
+    wave_prefix4(t0, t1, t2, t3, tc0, tc1, tc2, tc3);
+    const uint64_t S = read_lane(tc3, 63);
     uint32_t my_min = 0xFFFFFFFFu;  // smallest priority this wave selected
 
     for (int64_t b = wave_id; b < B; b += nwaves) {
@@ -213,40 +199,35 @@ __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict_
             if (lane == 0) {
                 idx[b] = -1;
                 start[b] = 0;
+                if (want_min) sel_prio[b] = 0u;
                 atomicOr(status, GEAR_STATUS_NO_WEIGHT);
             }
             continue;
         }
-        const uint64_t r = scale_draw(splitmix64_out(seed, 2 * (uint64_t)b), S);
-        uint64_t lo = 0;
-        int64_t j = 0;
-        for (int l = top; l >= 0; l--) j = descend_level(lv.level[l], lv.size[l], j * kFanout, r, lane, lo);
-
-        // j is the tile holding r; scan its 256 priorities in registers.
-        const uint64_t rr = r - lo;
-        const int64_t e = j * kTile + lane * 4;
-        uint32_t p0, p1, p2, p3;
-        if (e + 4 <= N) {
-            const uint4 v = *reinterpret_cast<const uint4*>(prio + e);
-            p0 = v.x; p1 = v.y; p2 = v.z; p3 = v.w;
-        } else {
-            p0 = e + 0 < N ? prio[e + 0] : 0u;
-            p1 = e + 1 < N ? prio[e + 1] : 0u;
-            p2 = e + 2 < N ? prio[e + 2] : 0u;
-            p3 = e + 3 < N ? prio[e + 3] : 0u;
+        uint64_t r = scale_draw(splitmix64_out(seed, 2 * (uint64_t)b), S);
+        int64_t j = pick_child(tc0, tc1, tc2, tc3, r);
+        for (int l = top - 1; l >= 0; l--) {
+            uint64_t v0, v1, v2, v3, c0, c1, c2, c3;
+            load4_u64(lv.level[l], lv.size[l], j * kFanout + lane * 4, v0, v1, v2, v3);
+            wave_prefix4(v0, v1, v2, v3, c0, c1, c2, c3);
+            j = j * kFanout + pick_child(c0, c1, c2, c3, r);
         }
-        const uint64_t lsum = (uint64_t)p0 + p1 + p2 + p3;
-        const uint64_t excl = wave_inclusive_scan(lsum, lane) - lsum;
-        const uint64_t c0 = excl + p0, c1 = c0 + p1, c2 = c1 + p2, c3 = c2 + p3;
-        const int cnt = __popcll(__ballot(c0 <= rr)) + __popcll(__ballot(c1 <= rr)) +
-                        __popcll(__ballot(c2 <= rr)) + __popcll(__ballot(c3 <= rr));
+        // j is the tile holding r: the same over its 256 priorities.
+        uint32_t p0, p1, p2, p3;
+        uint64_t c0, c1, c2, c3;
+        load4_u32(prio, N, j * kTile + lane * 4, p0, p1, p2, p3);
+        wave_prefix4(p0, p1, p2, p3, c0, c1, c2, c3);
+        const int cnt = pick_child(c0, c1, c2, c3, r);
         if (lane == 0) {
             idx[b] = j * kTile + cnt;
             start[b] = (int32_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b + 1), span);
         }
         if (want_min) {
-            const uint32_t pv = (uint32_t)__shfl((uint64_t)pick4(p0, p1, p2, p3, cnt & 3), cnt >> 2);
+            // The selected priority is kept for the weight kernel in the
+            // caller's weight buffer, which that kernel then overwrites.
+            const uint32_t pv = (uint32_t)read_lane(pick4(p0, p1, p2, p3, cnt & 3), cnt >> 2);
             my_min = pv < my_min ? pv : my_min;
+            if (lane == 0) sel_prio[b] = pv;
         }
     }
     if (want_min) {
@@ -263,12 +244,14 @@ __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict_
 
 // w_b = (n*P(i_b))^-beta / max_b' (n*P(i_b'))^-beta = (p_min / p_b)^beta,
 // p_min the smallest selected priority; fp64, rounded once to fp32.  Every
-// workgroup first reduces the search's per-workgroup minima.
-__global__ __launch_bounds__(256) void is_weights_kernel(const uint32_t* __restrict__ prio, int64_t N,
-                                                         const int64_t* __restrict__ idx, int32_t B, double beta,
-                                                         const uint32_t* __restrict__ wg_min, int search_grid,
-                                                         float* __restrict__ w) {
+// workgroup first reduces the search's per-workgroup minima.  The selected
+// priority p_b arrives in w[b] itself (as uint32 bits; 0 marks a draw with
+// no selectable slot) and is replaced by the weight.
+__global__ __launch_bounds__(256) void is_weights_kernel(int32_t B, double beta, const uint32_t* __restrict__ wg_min,
+                                                         int search_grid, float* __restrict__ w) {
     __shared__ uint32_t s_min[4];
+    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint32_t pb = b < B ? reinterpret_cast<const uint32_t*>(w)[b] : 0u;
     uint32_t m = 0xFFFFFFFFu;
     for (int k = threadIdx.x; k < search_grid; k += blockDim.x) m = wg_min[k] < m ? wg_min[k] : m;
 #pragma unroll
@@ -280,15 +263,8 @@ __global__ __launch_bounds__(256) void is_weights_kernel(const uint32_t* __restr
     __syncthreads();
     m = s_min[0];
     for (int k = 1; k < (int)(blockDim.x >> 6); k++) m = s_min[k] < m ? s_min[k] : m;
-
-    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= B) return;
-    const int64_t i = idx[b];
-    if (i < 0 || i >= N || m == 0u) {
-        w[b] = 0.0f;
-        return;
-    }
-    w[b] = (float)pow((double)m / (double)prio[i], beta);
+    w[b] = (pb == 0u || m == 0u) ? 0.0f : (float)pow((double)m / (double)pb, beta);
 }
 
 // FIFO / LIFO: ring arithmetic from the oldest / newest live slot.
@@ -313,43 +289,54 @@ __global__ void simple_select_kernel(int strategy, int32_t B, int64_t N, int64_t
     if (w) w[b] = 1.0f;
 }
 
-Levels make_levels(const Table& t) {
+// The tree as the search sees it: level 0 and the copy of the upper levels
+// that the last scan filled.
+Levels tree(const Table& t) {
     Levels lv{};
+    lv.nlevels = t.nlevels;
     for (int l = 0; l < t.nlevels; l++) {
-        lv.level[l] = t.level[l];
+        lv.level[l] = l == 0 ? t.tile_sums : t.upper[t.tree_parity][l];
         lv.size[l] = t.level_size[l];
     }
+    return lv;
+}
+
+Levels upper_copy(const Table& t, int parity) {
+    Levels lv{};
     lv.nlevels = t.nlevels;
+    for (int l = 1; l < t.nlevels; l++) {
+        lv.level[l] = t.upper[parity][l];
+        lv.size[l] = t.level_size[l];
+    }
     return lv;
 }
 
 }  // namespace
 
 hipError_t launch_scan(Table& t, hipStream_t s) {
-    const int par = t.scan_parity;
-    hipLaunchKernelGGL(scan_kernel, dim3((unsigned)t.nchunks), dim3(256), 0, s, t.priority, t.N, t.ntiles,
-                       make_levels(t), t.lookback + (size_t)par * t.nchunks,
-                       t.lookback + (size_t)(1 - par) * t.nchunks, t.ticket + par, t.ticket + (1 - par),
-                       t.nchunks, t.status);
+    // The copy this scan fills was zeroed by the previous scan (or at
+    // creation); this scan zeroes the other copy for the next one.
+    const int par = 1 - t.tree_parity;
+    hipLaunchKernelGGL(scan_kernel, dim3((unsigned)t.nchunks), dim3(256), 0, s, t.priority, t.N, upper_copy(t, par),
+                       upper_copy(t, 1 - par), t.tile_sums, t.ntiles);
     hipError_t e = hipGetLastError();
-    if (e == hipSuccess) t.scan_parity = 1 - par;
+    if (e == hipSuccess) t.tree_parity = par;
     return e;
 }
 
 hipError_t launch_search(Table& t, int32_t B, int32_t L, uint64_t seed, bool want_min, int64_t* idx,
-                         int32_t* start, int* grid_out, hipStream_t s) {
+                         int32_t* start, uint32_t* sel_prio, int* grid_out, hipStream_t s) {
     int64_t g = ((int64_t)B + 3) / 4;  // one wave per draw while the grid allows
     const int grid = (int)(g < kSearchMaxGrid ? g : kSearchMaxGrid);
-    hipLaunchKernelGGL(search_kernel, dim3(grid), dim3(256), 0, s, t.priority, t.N, make_levels(t), B,
-                       (uint64_t)(t.T - L + 1), seed, want_min ? 1 : 0, t.wg_min, t.status, idx, start);
+    hipLaunchKernelGGL(search_kernel, dim3(grid), dim3(256), 0, s, t.priority, t.N, tree(t), B,
+                       (uint64_t)(t.T - L + 1), seed, want_min ? 1 : 0, t.wg_min, t.status, idx, start, sel_prio);
     *grid_out = grid;
     return hipGetLastError();
 }
 
-hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, const int64_t* idx, float* w,
-                             hipStream_t s) {
-    hipLaunchKernelGGL(is_weights_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s, t.priority, t.N, idx,
-                       B, (double)beta, t.wg_min, search_grid, w);
+hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, float* w, hipStream_t s) {
+    hipLaunchKernelGGL(is_weights_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s, B, (double)beta,
+                       t.wg_min, search_grid, w);
     return hipGetLastError();
 }
 
@@ -396,10 +383,11 @@ extern "C" int gear_select(gear_table* h, int32_t strategy, int32_t B, int32_t L
     }
     const bool weights = d_weights != nullptr;
     int grid = 0;
-    hipError_t e = gear::launch_search(*t, B, L, seed, weights, d_idx, d_start, &grid, s);
+    hipError_t e = gear::launch_search(*t, B, L, seed, weights, d_idx, d_start,
+                                       reinterpret_cast<uint32_t*>(d_weights), &grid, s);
     if (e != hipSuccess) return hip_fail(e, "gear_select: search launch");
     if (weights) {
-        e = gear::launch_is_weights(*t, B, beta, grid, d_idx, d_weights, s);
+        e = gear::launch_is_weights(*t, B, beta, grid, d_weights, s);
         if (e != hipSuccess) return hip_fail(e, "gear_select: weight launch");
     }
     return GEAR_OK;

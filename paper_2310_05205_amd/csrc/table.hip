@@ -57,9 +57,9 @@ void free_table(Table* t) {
     }
     (void)hipFree(t->priority);
     (void)hipFree(t->tag);
-    for (int l = 0; l < gear::kMaxLevels; l++) (void)hipFree(t->level[l]);
-    (void)hipFree(t->lookback);
-    (void)hipFree(t->ticket);
+    (void)hipFree(t->tile_sums);
+    for (int c = 0; c < 2; c++)
+        for (int l = 0; l < gear::kMaxLevels; l++) (void)hipFree(t->upper[c][l]);
     (void)hipFree(t->wg_min);
     (void)hipFree(t->status);
     delete t;
@@ -144,7 +144,7 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
         }
     }
 
-    // Prefix tree geometry.
+    // Sum tree geometry.
     t->ntiles = (capacity + gear::kTile - 1) / gear::kTile;
     t->nchunks = (t->ntiles + gear::kTilesPerChunk - 1) / gear::kTilesPerChunk;
     int64_t sz = t->ntiles;
@@ -157,17 +157,22 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
     }
     if ((e = dmalloc(&t->priority, sizeof(uint32_t) * capacity)) != hipSuccess) return oom("priorities", e);
     if ((e = dmalloc(&t->tag, sizeof(uint32_t) * capacity)) != hipSuccess) return oom("scatter tags", e);
-    for (int l = 0; l < t->nlevels; l++)
-        if ((e = dmalloc(&t->level[l], sizeof(uint64_t) * t->level_size[l])) != hipSuccess) return oom("prefix levels", e);
-    if ((e = dmalloc(&t->lookback, sizeof(uint64_t) * 2 * t->nchunks)) != hipSuccess) return oom("look-back words", e);
-    if ((e = dmalloc(&t->ticket, sizeof(uint32_t) * 2)) != hipSuccess) return oom("tickets", e);
+    if ((e = dmalloc(&t->tile_sums, sizeof(uint64_t) * t->ntiles)) != hipSuccess) return oom("tile sums", e);
+    for (int c = 0; c < 2; c++)
+        for (int l = 1; l < t->nlevels; l++) {
+            if ((e = dmalloc(&t->upper[c][l], sizeof(uint64_t) * t->level_size[l])) != hipSuccess)
+                return oom("sum tree levels", e);
+            if ((e = hipMemset(t->upper[c][l], 0, sizeof(uint64_t) * t->level_size[l])) != hipSuccess) {
+                free_table(t);
+                return hip_fail(e, "gear_table_create: clearing the sum tree");
+            }
+        }
     if ((e = dmalloc(&t->wg_min, sizeof(uint32_t) * gear::kSearchMaxGrid)) != hipSuccess) return oom("batch minima", e);
     if ((e = dmalloc(&t->status, sizeof(uint32_t))) != hipSuccess) return oom("status word", e);
 
     if ((e = hipMemset(t->priority, 0, sizeof(uint32_t) * capacity)) != hipSuccess ||
         (e = hipMemset(t->tag, 0, sizeof(uint32_t) * capacity)) != hipSuccess ||
-        (e = hipMemset(t->lookback, 0, sizeof(uint64_t) * 2 * t->nchunks)) != hipSuccess ||
-        (e = hipMemset(t->ticket, 0, sizeof(uint32_t) * 2)) != hipSuccess ||
+        (e = hipMemset(t->tile_sums, 0, sizeof(uint64_t) * t->ntiles)) != hipSuccess ||
         (e = hipMemset(t->wg_min, 0xFF, sizeof(uint32_t) * gear::kSearchMaxGrid)) != hipSuccess ||
         (e = hipMemset(t->status, 0, sizeof(uint32_t))) != hipSuccess ||
         (e = hipDeviceSynchronize()) != hipSuccess) {

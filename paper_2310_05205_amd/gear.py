@@ -242,7 +242,7 @@ def _hip_memcpy_d2h(dst, src, nbytes):
     """Plain hipMemcpy for reading table state back (tests, checks)."""
     global _hip
     if _hip is None:
-        _hip = ctypes.CDLL("libamdhip64.so")
+        _hip = ctypes.CDLL("libamdhip64.so.7")  # the runtime libgear.so is bound to
         _hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
         _hip.hipMemcpy.restype = ctypes.c_int
     rc = _hip.hipMemcpy(dst, src, nbytes, 2)  # hipMemcpyDeviceToHost

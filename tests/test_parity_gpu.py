@@ -225,15 +225,18 @@ def test_more_than_sixteen_columns_and_subsets():
         t.close()
 
 
-def test_duplicate_heavy_update_last_wins():
-    w = _custom("dups", 100, 1, [], 100, U1000, 5000, 1)
+@pytest.mark.parametrize("B", [1, 5000, 8192, 8193, 20000])
+def test_duplicate_heavy_update_last_wins(B):
+    # B <= 8192 runs the one-workgroup LDS path, larger B the two-kernel path.
+    w = _custom("dups", 100, 1, [], 100, U1000, B, 1)
     p, _ = oracle_priorities(w)
     t = gpu_table(w)
     try:
-        rng = np.random.default_rng(3)
+        rng = np.random.default_rng(B)
         for it in range(5):
-            idx = rng.integers(0, w.N, size=5000)
-            newp = rng.integers(1, 1 << 32, size=5000, dtype=np.uint64).astype(np.uint32)
+            say("dups B=%d iteration %d" % (B, it))
+            idx = rng.integers(0, w.N, size=B)
+            newp = rng.integers(1, 1 << 32, size=B, dtype=np.uint64).astype(np.uint32)
             t.update_priorities(torch.from_numpy(idx).to(cuda()), torch.from_numpy(newp).to(cuda()))
             oracle.update(p, idx, newp)
             np.testing.assert_array_equal(t.priorities(), p)
