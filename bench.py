@@ -15,6 +15,7 @@ sample of the same workload.
 
   python bench.py [--steps K] [--warmup W] [--workload mat|gato-host|dt|tiny|select-stress]
   python bench.py --calibrate     # plain copy kernel of known size, for counter scaling
+  python bench.py --ceilings      # HBM read / write / copy rates of plain kernels
 """
 import argparse
 import ctypes
@@ -83,6 +84,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target oracle time for the CPU baseline")
     ap.add_argument("--calibrate", action="store_true", help="run a plain copy kernel of known size and exit")
+    ap.add_argument("--ceilings", action="store_true", help="measure plain read/write/copy HBM rates and exit")
     return ap.parse_args()
 
 
@@ -104,6 +106,36 @@ def calibrate():
     torch.cuda.synchronize()
     print(json.dumps({"calibrate": "bitwise_not int64", "bytes_read_per_launch": n * 8,
                       "bytes_written_per_launch": n * 8, "launches": 5}))
+
+
+def ceilings():
+    """HBM rates of plain torch kernels on 8 GiB buffers (no gather, no
+    replay): a read-only reduction, a fill, and an elementwise copy.  They
+    bound what a kernel that reads and writes HBM can reach on this device."""
+    import torch
+    n = (8 << 30) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    sh = torch.cuda.current_stream().cuda_stream
+    hev = HipEvents()
+    out = {}
+    tests = [("read (sum)", lambda: torch.sum(a), n * 4),
+             ("write (fill)", lambda: b.fill_(2.0), n * 4),
+             ("copy (neg)", lambda: torch.neg(a, out=b), 2 * n * 4)]
+    for name, fn, nbytes in tests:
+        for _ in range(3):
+            fn()
+        e0, e1 = hev.create(), hev.create()
+        hev.record(e0, sh)
+        for _ in range(10):
+            fn()
+        hev.record(e1, sh)
+        torch.cuda.synchronize()
+        ms = hev.elapsed_ms(e0, e1) / 10
+        out[name] = {"GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1), "ms": round(ms, 4),
+                     "frac_of_8TB/s": round(nbytes / (ms * 1e-3) / 8e12, 4)}
+    hev.close()
+    print(json.dumps({"ceilings": out, "bytes_per_buffer": n * 4}))
 
 
 def source_sha(path):
@@ -177,6 +209,9 @@ def main():
         sys.exit(2)
     if args.calibrate:
         calibrate()
+        return
+    if args.ceilings:
+        ceilings()
         return
 
     import numpy as np
