@@ -82,6 +82,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="mat", choices=["mat", "gato-host", "dt", "tiny", "select-stress"])
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
+    ap.add_argument("--incremental", action="store_true",
+                    help="keep the selection sum tree current across updates (no rescan per step)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target oracle time for the CPU baseline")
     ap.add_argument("--calibrate", action="store_true", help="run a plain copy kernel of known size and exit")
     ap.add_argument("--ceilings", action="store_true", help="measure plain read/write/copy HBM rates and exit")
@@ -232,6 +234,8 @@ def main():
     host_table = w.host_table
     t = gear.Table(w.elem_bytes, w.N, w.T, gear.GEAR_HOST_PINNED if host_table else gear.GEAR_DEVICE, 0)
     fill_table(w, lambda n, ptrs, prio: t.insert(ptrs, prio), device=0)
+    if args.incremental:
+        t.set_options(gear.GEAR_OPT_INCREMENTAL_TREE)
 
     K, W = args.steps, args.warmup
     B, L = w.B, w.L
@@ -334,7 +338,8 @@ def main():
                    "elem_bytes": w.elem_bytes, "table_bytes": w.table_bytes,
                    "residency": "pinned-host" if host_table else "hbm",
                    "strategy": {0: "fifo", 1: "lifo", 2: "uniform", 3: "prioritized"}[strategy],
-                   "is_weights": bool(w.weights), "parallelism": "1 GPU"},
+                   "is_weights": bool(w.weights), "parallelism": "1 GPU",
+                   "tree": "incremental" if args.incremental else "rescan per select"},
         "roofline": roof,
         "cpu_baseline": cpu,
         "stages_ms": {"select": round(sel_ms, 5), "collect": round(col_ms, 5), "update": round(upd_ms, 5),

@@ -60,6 +60,9 @@ extern "C" {
 #define GEAR_UNIFORM      2
 #define GEAR_PRIORITIZED  3
 
+/* Table options (gear_table_set_options). */
+#define GEAR_OPT_INCREMENTAL_TREE 1u  /* updates maintain the selection sum tree in place */
+
 /* Limits. */
 #define GEAR_MAX_CAPACITY  (1ll << 30)  /* keeps every priority total below 2^62 */
 #define GEAR_MAX_COLUMNS   64

@@ -49,7 +49,8 @@ struct Table {
     int tree_parity = 0;              // copy filled by the last scan
     uint32_t* wg_min = nullptr;       // [kSearchMaxGrid] per-workgroup minimum selected priority
     uint32_t* status = nullptr;       // device status word
-    bool cdf_dirty = true;
+    bool cdf_dirty = true;            // the tree does not reflect the priorities
+    uint32_t options = 0;             // GEAR_OPT_* bits
 };
 
 // Thread-local error reporting.
@@ -75,7 +76,9 @@ hipError_t launch_search(Table& t, int32_t B, int32_t L, uint64_t seed, bool wan
 hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, float* w, hipStream_t s);
 hipError_t launch_simple_select(Table& t, int32_t strategy, int32_t B, int32_t L, uint64_t seed,
                                 int64_t* idx, int32_t* start, float* w, hipStream_t s);
-hipError_t launch_scatter(Table& t, const int64_t* idx, const uint32_t* newp, int32_t B,
+// With maintain_tree, the scatter also adds new - old of every changed
+// slot into the sum tree the last scan filled.
+hipError_t launch_scatter(Table& t, const int64_t* idx, const uint32_t* newp, int32_t B, bool maintain_tree,
                           hipStream_t s);
 
 }  // namespace gear

@@ -236,6 +236,13 @@ extern "C" int gear_insert(gear_table* h, int64_t n, const void* const* col_src,
     return GEAR_OK;
 }
 
+extern "C" int gear_table_set_options(gear_table* h, uint32_t options) {
+    if (h == nullptr) return fail(GEAR_E_INVAL, "gear_table_set_options: table is NULL");
+    if (options & ~GEAR_OPT_INCREMENTAL_TREE) return fail(GEAR_E_INVAL, "gear_table_set_options: unknown option bits");
+    reinterpret_cast<Table*>(h)->options = options;
+    return GEAR_OK;
+}
+
 extern "C" int gear_table_sync(gear_table* h, void* stream, int32_t* device_status) {
     if (h == nullptr) return fail(GEAR_E_INVAL, "gear_table_sync: table is NULL");
     Table* t = reinterpret_cast<Table*>(h);

@@ -29,6 +29,7 @@ GEAR_FIFO = 0
 GEAR_LIFO = 1
 GEAR_UNIFORM = 2
 GEAR_PRIORITIZED = 3
+GEAR_OPT_INCREMENTAL_TREE = 1
 
 
 class GearError(RuntimeError):
@@ -59,9 +60,10 @@ def lib():
         L.gear_table_info.argtypes = [vp, ctypes.POINTER(i64), ctypes.POINTER(u64)]
         L.gear_table_column.argtypes = [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(i64)]
         L.gear_table_priorities.argtypes = [vp, ctypes.POINTER(vp)]
+        L.gear_table_set_options.argtypes = [vp, ctypes.c_uint32]
         for name in ["gear_table_create", "gear_table_destroy", "gear_insert", "gear_select", "gear_collect",
                      "gear_update_priorities", "gear_table_sync", "gear_table_info", "gear_table_column",
-                     "gear_table_priorities"]:
+                     "gear_table_priorities", "gear_table_set_options"]:
             getattr(L, name).restype = ctypes.c_int
         L.gear_last_error.argtypes = []
         L.gear_last_error.restype = ctypes.c_char_p
@@ -140,6 +142,10 @@ def gear_table_column(table, c):
     return base.value, host.value, eb.value
 
 
+def gear_table_set_options(table, options):
+    _check(lib().gear_table_set_options(table, int(options)))
+
+
 def gear_table_priorities(table):
     p = ctypes.c_void_p()
     _check(lib().gear_table_priorities(table, ctypes.byref(p)))
@@ -209,6 +215,9 @@ class Table:
     def update_priorities(self, idx, new_priorities, stream=None):
         gear_update_priorities(self.handle, idx.data_ptr(), new_priorities.data_ptr(), int(idx.shape[0]),
                                self._stream(stream))
+
+    def set_options(self, options):
+        gear_table_set_options(self.handle, options)
 
     def sync(self, stream=None):
         return gear_table_sync(self.handle, self._stream(stream))

@@ -26,11 +26,13 @@ def host(t):
     return t.detach().cpu().numpy()
 
 
-def gpu_table(w, residency=None):
+def gpu_table(w, residency=None, options=0):
     """HIP-side table holding all of w's insertions."""
     if residency is None:
         residency = gear.GEAR_HOST_PINNED if w.host_table else gear.GEAR_DEVICE
     t = gear.Table(w.elem_bytes, w.N, w.T, residency, DEV)
+    if options:
+        t.set_options(options)
     fill_table(w, lambda n, ptrs, prio: t.insert(ptrs, prio), device=DEV)
     return t
 

@@ -51,10 +51,10 @@ def _check_table_contents(t, w, s):
     np.testing.assert_array_equal(t.priorities(), s.priority)
 
 
-def _run_full(w, iterations, strategies=None, check_contents=True):
+def _run_full(w, iterations, strategies=None, check_contents=True, options=0):
     """Full comparison on a workload small enough for a full oracle store."""
     s = oracle_store(w)
-    t = gpu_table(w)
+    t = gpu_table(w, options=options)
     try:
         if check_contents:
             _check_table_contents(t, w, s)
@@ -90,10 +90,11 @@ def test_tiny_prioritized_replay():
     _run_full(configs.TINY, iterations=5)
 
 
-def test_selection_stress_100_iterations():
+@pytest.mark.parametrize("options", [0, gear.GEAR_OPT_INCREMENTAL_TREE], ids=["rescan", "incremental"])
+def test_selection_stress_100_iterations(options):
     w = configs.SELECT_STRESS
     p, next_seq = oracle_priorities(w)
-    t = gpu_table(w)
+    t = gpu_table(w, options=options)
     try:
         np.testing.assert_array_equal(t.priorities(), p)
         for it in range(w.iterations):
@@ -172,18 +173,21 @@ EDGE = [
     _custom("lookback-depth", 300000, 1, [], 300000, U1000, 1024, 1),
     _custom("two-levels", (1 << 22) + 17, 1, [], (1 << 22) + 17, U1000, 4096, 1),
     _custom("three-levels", (1 << 24) + 5, 1, [], (1 << 24) + 5, U1000, 4096, 1),
+    _custom("wide-level1", (1 << 26) + 4097, 1, [], (1 << 26) + 4097, U1000, 4096, 1),
+    _custom("big-batch", 300000, 1, [], 300000, U1000, 12000, 1),
     _custom("wide-narrow-mix", 2000, 40, ODD, 2000, U1000, 700, 33),
     _custom("batch-one", 777, 6, ODD[:3], 777, U1000, 1, 6),
 ]
 
 
+@pytest.mark.parametrize("options", [0, gear.GEAR_OPT_INCREMENTAL_TREE], ids=["rescan", "incremental"])
 @pytest.mark.parametrize("w", EDGE, ids=[w.name for w in EDGE])
-def test_edge_cases(w):
+def test_edge_cases(w, options):
     big = w.N > 100000
     if big:
         # Selection-only shapes: compare without a full oracle store.
         p, next_seq = oracle_priorities(w)
-        t = gpu_table(w)
+        t = gpu_table(w, options=options)
         try:
             for it in range(3):
                 say("%s iteration %d" % (w.name, it))
@@ -200,7 +204,7 @@ def test_edge_cases(w):
         finally:
             t.close()
     else:
-        _run_full(w, iterations=3)
+        _run_full(w, iterations=3, options=options)
 
 
 def test_more_than_sixteen_columns_and_subsets():
@@ -225,12 +229,14 @@ def test_more_than_sixteen_columns_and_subsets():
         t.close()
 
 
+@pytest.mark.parametrize("options", [0, gear.GEAR_OPT_INCREMENTAL_TREE], ids=["rescan", "incremental"])
 @pytest.mark.parametrize("B", [1, 5000, 8192, 8193, 20000])
-def test_duplicate_heavy_update_last_wins(B):
-    # B <= 8192 runs the one-workgroup LDS path, larger B the two-kernel path.
+def test_duplicate_heavy_update_last_wins(B, options):
+    # B <= 8192 runs the one-launch LDS path, larger B the two-kernel path.
     w = _custom("dups", 100, 1, [], 100, U1000, B, 1)
-    p, _ = oracle_priorities(w)
-    t = gpu_table(w)
+    p, next_seq = oracle_priorities(w)
+    t = gpu_table(w, options=options)
+    t.select(3, 16, 1, 1)   # builds the tree, so updates maintain it when asked
     try:
         rng = np.random.default_rng(B)
         for it in range(5):
@@ -240,6 +246,9 @@ def test_duplicate_heavy_update_last_wins(B):
             t.update_priorities(torch.from_numpy(idx).to(cuda()), torch.from_numpy(newp).to(cuda()))
             oracle.update(p, idx, newp)
             np.testing.assert_array_equal(t.priorities(), p)
+            sel, _, _ = t.select(3, 4096, 1, 100 + it)
+            _, osel, _, _ = oracle.select(3, p, next_seq, 1, 4096, 1, 100 + it)
+            np.testing.assert_array_equal(host(sel), osel)
         assert t.sync() == 0
     finally:
         t.close()
@@ -322,9 +331,9 @@ def test_device_status_and_host_errors():
 # Full-size workloads, in the launch configuration the benchmark times.
 # ---------------------------------------------------------------------------
 
-def _full_size(w, iterations, sample_n):
+def _full_size(w, iterations, sample_n, options=0):
     p, next_seq = oracle_priorities(w)
-    t = gpu_table(w)
+    t = gpu_table(w, options=options)
     rng = np.random.default_rng(w.seed)
     try:
         for it in range(iterations):
@@ -356,5 +365,6 @@ def test_gato_pinned_host_zero_copy_full_size():
     _full_size(configs.GATO_HOST, iterations=2, sample_n=64)
 
 
-def test_mat_end_to_end_full_size():
-    _full_size(configs.MAT, iterations=2, sample_n=256)
+@pytest.mark.parametrize("options", [0, gear.GEAR_OPT_INCREMENTAL_TREE], ids=["rescan", "incremental"])
+def test_mat_end_to_end_full_size(options):
+    _full_size(configs.MAT, iterations=3, sample_n=256, options=options)
