@@ -80,7 +80,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="mat", choices=["mat", "gato-host", "dt", "tiny", "select-stress"])
+    ap.add_argument("--workload", default="mat", choices=["mat", "gato-host", "dt", "tiny", "select-stress", "topk"])
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
     ap.add_argument("--incremental", action="store_true",
                     help="keep the selection sum tree current across updates (no rescan per step)")
@@ -93,7 +93,7 @@ def parse():
 def workload(name):
     from gen import configs
     return {"mat": configs.MAT, "gato-host": configs.GATO_HOST, "dt": configs.DT, "tiny": configs.TINY,
-            "select-stress": configs.SELECT_STRESS}[name]
+            "select-stress": configs.SELECT_STRESS, "topk": configs.TOPK_STRESS}[name]
 
 
 def calibrate():
@@ -178,7 +178,8 @@ def cpu_baseline(w, target_s):
 
     p, next_seq = oracle_priorities(w)
     seed = gen.select_seed(w.seed, 0)
-    st, idx, start, _ = oracle.select(oracle.PRIORITIZED, p, next_seq, w.T, w.B, w.L, seed, w.beta, True)
+    strat = w.strategies[0]
+    st, idx, start, _ = oracle.select(strat, p, next_seq, w.T, w.B, w.L, seed, w.beta, True)
     assert st == oracle.OK
     ks = gen.slot_insertion(idx, next_seq, w.N)
     rows = [gen.fill_rows_list_cpu(c, ci, w.seed, w.T, ks) for ci, c in enumerate(w.columns)]
@@ -187,7 +188,7 @@ def cpu_baseline(w, target_s):
     reps = 0
     t0 = time.perf_counter()
     while True:
-        st, oidx, ostart, ow = oracle.select(oracle.PRIORITIZED, p, next_seq, w.T, w.B, w.L, seed, w.beta, True)
+        st, oidx, ostart, ow = oracle.select(strat, p, next_seq, w.T, w.B, w.L, seed, w.beta, True)
         if rows:
             st2, outs = oracle.collect(rows, w.T, local, ostart, w.L)
             del outs
@@ -197,9 +198,10 @@ def cpu_baseline(w, target_s):
         if el >= target_s:
             break
     return {"value": w.B * w.L * reps / el, "unit": "trajectory-steps/s", "cores": 1, "kind": "oracle",
-            "sample": "%d repetitions of one step (select over all %d priorities with IS weights, collect of "
+            "sample": "%d repetitions of one step (%s select over all %d priorities, collect of "
                       "the %d selected %d-step windows from a compact host table of the selected "
-                      "trajectories, update) in %.1f s on one host core" % (reps, w.N, w.B, w.L, el)}
+                      "trajectories, update) in %.1f s on one host core"
+                      % (reps, {3: "prioritized", 4: "TopK"}.get(strat, "select"), w.N, w.B, w.L, el)}
 
 
 def main():
@@ -240,7 +242,7 @@ def main():
     K, W = args.steps, args.warmup
     B, L = w.B, w.L
     strategy = w.strategies[0]
-    prioritized = strategy == gear.GEAR_PRIORITIZED
+    prioritized = strategy in (gear.GEAR_PRIORITIZED, gear.GEAR_TOPK)  # steps that update priorities
     idx = torch.empty(B, dtype=torch.int64, device=dev)
     start = torch.empty(B, dtype=torch.int32, device=dev)
     wts = torch.empty(B, dtype=torch.float32, device=dev)
@@ -337,7 +339,7 @@ def main():
                    "columns": {c.name: "%s[%d]" % (c.dtype, c.m) for c in w.columns},
                    "elem_bytes": w.elem_bytes, "table_bytes": w.table_bytes,
                    "residency": "pinned-host" if host_table else "hbm",
-                   "strategy": {0: "fifo", 1: "lifo", 2: "uniform", 3: "prioritized"}[strategy],
+                   "strategy": {0: "fifo", 1: "lifo", 2: "uniform", 3: "prioritized", 4: "topk"}[strategy],
                    "is_weights": bool(w.weights), "parallelism": "1 GPU",
                    "tree": "incremental" if args.incremental else "rescan per select"},
         "roofline": roof,

@@ -13,7 +13,7 @@ from typing import List, Optional, Tuple
 from . import (BYTES, DONE_U8, INT_MOD, NORMAL_BF16, NORMAL_F32, PRIO_LOGNORMAL, PRIO_PARETO,
                PRIO_UNIFORM, RTG_F32, STAMP, UNIFORM_F32, Column, PrioDist)
 
-FIFO, LIFO, UNIFORM, PRIORITIZED = 0, 1, 2, 3
+FIFO, LIFO, UNIFORM, PRIORITIZED, TOPK = 0, 1, 2, 3, 4
 
 
 @dataclass(frozen=True)
@@ -95,4 +95,11 @@ MAT = Workload(
     n_insert=500000, prio=PrioDist(PRIO_LOGNORMAL, 6.931471805599453, 1.0, float(1 << 24)),
     strategies=(PRIORITIZED,), B=8192, L=32, weights=True, iterations=20)
 
-ALL = (TINY, DT, SELECT_STRESS, GATO_HOST, MAT)
+# TopK over the selection-stress priorities: the 8192 highest of 2^22.
+TOPK_STRESS = Workload(
+    name="topk-stress N=4194304 K=8192",
+    seed=3, N=1 << 22, T=1, columns=(),
+    n_insert=1 << 22, prio=PrioDist(PRIO_PARETO, 1.5, float(1 << 24)),
+    strategies=(TOPK,), B=8192, L=1, weights=False, iterations=100)
+
+ALL = (TINY, DT, SELECT_STRESS, GATO_HOST, MAT, TOPK_STRESS)

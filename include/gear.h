@@ -59,6 +59,7 @@ extern "C" {
 #define GEAR_LIFO         1
 #define GEAR_UNIFORM      2
 #define GEAR_PRIORITIZED  3
+#define GEAR_TOPK         4  /* deterministic: the highest priorities (Sec. 3.3, decentralized selection) */
 
 /* Table options (gear_table_set_options). */
 #define GEAR_OPT_INCREMENTAL_TREE 1u  /* updates maintain the selection sum tree in place */
@@ -67,6 +68,7 @@ extern "C" {
 #define GEAR_MAX_CAPACITY  (1ll << 30)  /* keeps every priority total below 2^62 */
 #define GEAR_MAX_COLUMNS   64
 #define GEAR_MAX_BATCH     (1 << 24)
+#define GEAR_MAX_TOPK      16384        /* B limit of GEAR_TOPK */
 
 typedef struct gear_table gear_table;
 
@@ -129,7 +131,13 @@ int gear_insert(gear_table *t, int64_t n, const void *const *col_src, const uint
  *             GEAR_UNIFORM: B draws with replacement, uniform over live slots.
  *             GEAR_PRIORITIZED: B draws with replacement, slot i with
  *             probability p_i / S, S the sum of all priorities.
- *   B         1 .. GEAR_MAX_BATCH (FIFO/LIFO: at most the live count)
+ *             GEAR_TOPK: the B slots with the highest non-zero priorities,
+ *             higher priority first and the lower slot first among equal
+ *             priorities; if fewer than B slots have non-zero priority the
+ *             remaining draws get idx = -1, start = 0, weight 0 and
+ *             GEAR_STATUS_NO_WEIGHT is set.
+ *   B         1 .. GEAR_MAX_BATCH (FIFO/LIFO: at most the live count;
+ *             TOPK: at most GEAR_MAX_TOPK)
  *   L         window length in steps, 1 .. T
  *   seed      draw b uses splitmix64 outputs 2b (index) and 2b+1 (start) of
  *             the stream seeded with `seed`; a draw is floor(u * n / 2^64)

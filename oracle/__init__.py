@@ -19,7 +19,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-FIFO, LIFO, UNIFORM, PRIORITIZED = 0, 1, 2, 3
+FIFO, LIFO, UNIFORM, PRIORITIZED, TOPK = 0, 1, 2, 3, 4
 OK, INVAL, EMPTY, INSUFFICIENT, NO_WEIGHT = 0, -1, -3, -4, -6
 
 

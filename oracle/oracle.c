@@ -44,6 +44,7 @@
 #include <stddef.h>
 #include <string.h>
 #include <math.h>
+#include <stdlib.h>
 
 /* Oracle status codes (the oracle's own; deliberately not shared). */
 #define ORC_OK            0
@@ -56,6 +57,7 @@
 #define ORC_LIFO        1
 #define ORC_UNIFORM     2
 #define ORC_PRIORITIZED 3
+#define ORC_TOPK        4
 
 /* ------------------------------------------------------------------------ */
 /* splitmix64 (Steele, Lea & Flood, "Fast splittable pseudorandom number     */
@@ -119,6 +121,24 @@ int64_t oracle_upper_bound(const uint64_t *C, int64_t n, uint64_t r)
 }
 
 /* ------------------------------------------------------------------------ */
+/* TopK order (Sec. 3.3, decentralized selection: the top-K priority          */
+/* trajectories): higher priority first, the lower slot first among equal     */
+/* priorities.                                                               */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    uint32_t p;
+    int64_t i;
+} orc_cand;
+
+static int orc_topk_cmp(const void *a, const void *b)
+{
+    const orc_cand *x = (const orc_cand *)a, *y = (const orc_cand *)b;
+    if (x->p != y->p)
+        return x->p > y->p ? -1 : 1;
+    return x->i < y->i ? -1 : (x->i > y->i ? 1 : 0);
+}
+
+/* ------------------------------------------------------------------------ */
 /* Selection (Sec. 1 strategies; Sec. 3.3).                                   */
 /*                                                                          */
 /* State of the store: capacity N slots, `next_seq` insertions so far, the  */
@@ -142,7 +162,7 @@ int oracle_select(int strategy, const uint32_t *priority, int64_t N,
 
     if (N <= 0 || T <= 0 || B <= 0 || L <= 0 || L > T || idx == NULL || start == NULL)
         return ORC_INVAL;
-    if (strategy < ORC_FIFO || strategy > ORC_PRIORITIZED)
+    if (strategy < ORC_FIFO || strategy > ORC_TOPK)
         return ORC_INVAL;
     n = (next_seq < (uint64_t)N) ? (int64_t)next_seq : N;
     if (n == 0)
@@ -165,6 +185,32 @@ int oracle_select(int strategy, const uint32_t *priority, int64_t N,
         /* Uniform over the live slots [0, n). */
         for (b = 0; b < B; b++)
             idx[b] = (int64_t)oracle_bounded(oracle_draw(seed, 2u * (uint64_t)b), (uint64_t)n);
+    } else if (strategy == ORC_TOPK) {
+        /* The B highest-priority selectable slots (priority > 0), higher
+         * priority first, lower slot first among equals.  Missing draws
+         * (fewer than B selectable slots) get slot -1 and weight 0. */
+        int64_t ncand = 0, i;
+        orc_cand *cand = (orc_cand *)malloc(sizeof(orc_cand) * (size_t)(N > 0 ? N : 1));
+        if (cand == NULL)
+            return ORC_INVAL;
+        for (i = 0; i < N; i++) {
+            if (priority[i] > 0) {
+                cand[ncand].p = priority[i];
+                cand[ncand].i = i;
+                ncand++;
+            }
+        }
+        qsort(cand, (size_t)ncand, sizeof(orc_cand), orc_topk_cmp);
+        for (b = 0; b < B; b++)
+            idx[b] = (int64_t)b < ncand ? cand[b].i : -1;
+        free(cand);
+        if (w != NULL)
+            for (b = 0; b < B; b++)
+                w[b] = idx[b] >= 0 ? 1.0f : 0.0f;
+        for (b = 0; b < B; b++)
+            start[b] = idx[b] >= 0 ? (int32_t)oracle_bounded(oracle_draw(seed, 2u * (uint64_t)b + 1u),
+                                                             (uint64_t)(T - L + 1)) : 0;
+        return ncand >= (int64_t)B ? ORC_OK : ORC_NO_WEIGHT;
     } else {
         /* Weighted: prefix sum over all N priorities, then one upper-bound
          * search per uniform number r in [0, S). */

@@ -23,6 +23,10 @@ constexpr int kMaxLevels = 6;
 // The search runs at most this many workgroups; each leaves the smallest
 // priority its draws selected in one slot of Table::wg_min.
 constexpr int kSearchMaxGrid = 2048;
+// TopK: at most this many workgroups per pass, and at most this many draws
+// (the final sort holds all K keys in one workgroup's LDS).
+constexpr int kTopkMaxGrid = 128;
+constexpr int kTopkMaxK = GEAR_MAX_TOPK;
 
 struct Table {
     int device = 0;
@@ -51,6 +55,13 @@ struct Table {
     uint32_t* status = nullptr;       // device status word
     bool cdf_dirty = true;            // the tree does not reflect the priorities
     uint32_t options = 0;             // GEAR_OPT_* bits
+
+    // TopK scratch (fixed sizes).
+    uint32_t* topk_hist = nullptr;    // [3][2048] digit histograms, zero between calls
+    uint32_t* topk_state = nullptr;   // [3][4] per-pass selection state
+    uint32_t* topk_ticket = nullptr;  // [3] per-pass workgroup tickets, zero between calls
+    uint32_t* topk_counts = nullptr;  // [2][kTopkMaxGrid] per-workgroup counts above / at the threshold
+    uint64_t* topk_keys = nullptr;    // [kTopkMaxK] selected keys before sorting
 };
 
 // Thread-local error reporting.
@@ -74,6 +85,8 @@ hipError_t launch_scan(Table& t, hipStream_t s);
 hipError_t launch_search(Table& t, int32_t B, int32_t L, uint64_t seed, bool want_min,
                          int64_t* idx, int32_t* start, uint32_t* sel_prio, int* grid_out, hipStream_t s);
 hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, float* w, hipStream_t s);
+hipError_t launch_topk(Table& t, int32_t K, int32_t L, uint64_t seed, int64_t* idx, int32_t* start, float* w,
+                       hipStream_t s);
 hipError_t launch_simple_select(Table& t, int32_t strategy, int32_t B, int32_t L, uint64_t seed,
                                 int64_t* idx, int32_t* start, float* w, hipStream_t s);
 // With maintain_tree, the scatter also adds new - old of every changed

@@ -25,6 +25,7 @@
 //
 // FIFO, LIFO and uniform selection are one thread per draw.
 #include "gear_internal.h"
+#include "wave.h"
 
 namespace gear {
 namespace {
@@ -34,53 +35,6 @@ struct Levels {
     int64_t size[kMaxLevels];
     int nlevels;
 };
-
-// splitmix64 (Steele, Lea & Flood, OOPSLA 2014): output c of the stream
-// seeded with `seed` is the finaliser applied to seed + (c+1)*gamma.
-__device__ inline uint64_t splitmix64_out(uint64_t seed, uint64_t c) {
-    uint64_t z = seed + (c + 1) * 0x9E3779B97F4A7C15ull;
-    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
-    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
-    return z ^ (z >> 31);
-}
-
-// floor(u * n / 2^64): the high word of the 128-bit product.
-__device__ inline uint64_t scale_draw(uint64_t u, uint64_t n) { return __umul64hi(u, n); }
-
-// Wave-level scans with DPP (gfx9 data-parallel primitives, all 64 lanes
-// active): row shifts by 1, 2, 4, 8 scan each row of 16 lanes, then the
-// row broadcasts of lanes 15 and 31 carry row totals forward.  A lane whose
-// DPP source is outside its row receives 0.  64-bit values move as two
-// 32-bit halves.
-template <int CTRL, int ROW_MASK>
-__device__ inline uint64_t dpp_u64(uint64_t v) {
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, ROW_MASK, 0xf, false);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, ROW_MASK, 0xf, false);
-    return ((uint64_t)hi << 32) | lo;
-}
-
-__device__ inline uint64_t wave_inclusive_scan(uint64_t v) {
-    v += dpp_u64<0x111, 0xf>(v);  // row_shr:1
-    v += dpp_u64<0x112, 0xf>(v);  // row_shr:2
-    v += dpp_u64<0x114, 0xf>(v);  // row_shr:4
-    v += dpp_u64<0x118, 0xf>(v);  // row_shr:8
-    v += dpp_u64<0x142, 0xa>(v);  // row_bcast:15 into rows 1 and 3
-    v += dpp_u64<0x143, 0xc>(v);  // row_bcast:31 into rows 2 and 3
-    return v;
-}
-
-// Value of v in lane `src` (src is the same in every lane).
-__device__ inline uint64_t read_lane(uint64_t v, int src) {
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, src);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), src);
-    return ((uint64_t)hi << 32) | lo;
-}
-
-__device__ inline uint64_t wave_sum(uint64_t v) { return read_lane(wave_inclusive_scan(v), 63); }
-
-__device__ inline uint64_t pick4(uint64_t a, uint64_t b, uint64_t c, uint64_t d, int q) {
-    return q == 0 ? a : (q == 1 ? b : (q == 2 ? c : d));
-}
 
 // Inclusive prefix of 256 values held four per lane (lane l holds values
 // 4l..4l+3): c0..c3 receive the prefix at this lane's four positions.
@@ -359,7 +313,8 @@ extern "C" int gear_select(gear_table* h, int32_t strategy, int32_t B, int32_t L
                            int64_t* d_idx, int32_t* d_start, float* d_weights, void* stream) {
     if (h == nullptr) return fail(GEAR_E_INVAL, "gear_select: table is NULL");
     gear::Table* t = reinterpret_cast<gear::Table*>(h);
-    if (strategy < GEAR_FIFO || strategy > GEAR_PRIORITIZED) return fail(GEAR_E_INVAL, "gear_select: unknown strategy");
+    if (strategy < GEAR_FIFO || strategy > GEAR_TOPK) return fail(GEAR_E_INVAL, "gear_select: unknown strategy");
+    if (strategy == GEAR_TOPK && B > GEAR_MAX_TOPK) return fail(GEAR_E_INVAL, "gear_select: TopK batch above GEAR_MAX_TOPK");
     if (B < 1 || B > GEAR_MAX_BATCH) return fail(GEAR_E_INVAL, "gear_select: B out of range");
     if (L < 1 || L > t->T) return fail(GEAR_E_INVAL, "gear_select: L must lie in [1, T]");
     if (d_idx == nullptr || d_start == nullptr) return fail(GEAR_E_INVAL, "gear_select: output pointer is NULL");
@@ -372,6 +327,10 @@ extern "C" int gear_select(gear_table* h, int32_t strategy, int32_t B, int32_t L
     if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_select: hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
 
+    if (strategy == GEAR_TOPK) {
+        hipError_t e = gear::launch_topk(*t, B, L, seed, d_idx, d_start, d_weights, s);
+        return e == hipSuccess ? GEAR_OK : hip_fail(e, "gear_select: TopK launch");
+    }
     if (strategy != GEAR_PRIORITIZED) {
         hipError_t e = gear::launch_simple_select(*t, strategy, B, L, seed, d_idx, d_start, d_weights, s);
         return e == hipSuccess ? GEAR_OK : hip_fail(e, "gear_select: launch");

@@ -29,6 +29,8 @@ GEAR_FIFO = 0
 GEAR_LIFO = 1
 GEAR_UNIFORM = 2
 GEAR_PRIORITIZED = 3
+GEAR_TOPK = 4
+GEAR_MAX_TOPK = 16384
 GEAR_OPT_INCREMENTAL_TREE = 1
 
 

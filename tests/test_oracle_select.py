@@ -193,3 +193,39 @@ def test_select_errors():
     assert oracle.select(9, p, 8, 4, 2, 1, 0)[0] == oracle.INVAL
     st, idx, _, _ = oracle.select(oracle.PRIORITIZED, p, 8, 4, 50, 1, 0)
     assert st == oracle.OK and np.all(idx == 3)
+
+
+def _topk_numpy(p, K):
+    """TopK by numpy's lexsort: priority descending, then slot ascending,
+    among slots with non-zero priority."""
+    cand = np.nonzero(p)[0]
+    order = np.lexsort((cand, -p[cand].astype(np.int64)))
+    sel = cand[order][:K]
+    return np.concatenate([sel, -np.ones(K - sel.size, dtype=np.int64)])
+
+
+@pytest.mark.parametrize("N,K,hi", [(1, 1, 5), (300, 64, 3), (5000, 777, 1000), (4096, 4096, 2), (100000, 8192, 1 << 32)])
+def test_topk_matches_lexsort(N, K, hi):
+    rng = np.random.default_rng(N + K)
+    p = rng.integers(0, hi, size=N, dtype=np.uint64).astype(np.uint32)   # zeros and many ties
+    T, L = 10, 3
+    st, idx, start, w = oracle.select(oracle.TOPK, p, N, T, K, L, 12345, 0.0, True)
+    ref = _topk_numpy(p, K)
+    np.testing.assert_array_equal(idx, ref)
+    assert st == (oracle.OK if np.count_nonzero(p) >= K else oracle.NO_WEIGHT)
+    valid = idx >= 0
+    assert np.all(w[valid] == 1.0) and np.all(w[~valid] == 0.0)
+    expect = [(oracle.draw(12345, 2 * b + 1) * (T - L + 1)) >> 64 for b in range(K)]
+    np.testing.assert_array_equal(start[valid], np.array(expect)[valid])
+    assert np.all(start[~valid] == 0)
+
+
+def test_topk_brute_force_small():
+    # Every permutation-free check: the selected set is the K largest, ordered,
+    # and no unselected slot beats a selected one.
+    p = np.array([4, 0, 4, 1, 9, 4, 0, 2, 9, 1], dtype=np.uint32)
+    st, idx, _, _ = oracle.select(oracle.TOPK, p, p.size, 1, 6, 1, 0)
+    assert st == oracle.OK
+    assert list(idx) == [4, 8, 0, 2, 5, 7]
+    st, idx, _, _ = oracle.select(oracle.TOPK, p, p.size, 1, 9, 1, 0)
+    assert st == oracle.NO_WEIGHT and list(idx) == [4, 8, 0, 2, 5, 7, 3, 9, -1]

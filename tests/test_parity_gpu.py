@@ -368,3 +368,52 @@ def test_gato_pinned_host_zero_copy_full_size():
 @pytest.mark.parametrize("options", [0, gear.GEAR_OPT_INCREMENTAL_TREE], ids=["rescan", "incremental"])
 def test_mat_end_to_end_full_size(options):
     _full_size(configs.MAT, iterations=3, sample_n=256, options=options)
+
+
+# ---------------------------------------------------------------------------
+# TopK selection (deterministic: highest priorities, lower slot on ties).
+# ---------------------------------------------------------------------------
+
+TOPK_CASES = [
+    _custom("topk-one", 1, 3, [], 1, U1000, 1, 2, strategies=(4,)),
+    _custom("topk-ties", 1000, 3, [], 1000, gen.PrioDist(gen.PRIO_UNIFORM, 1, 3), 777, 2, strategies=(4,)),
+    _custom("topk-short", 4097, 2, [], 300, U1000, 1024, 1, strategies=(4,)),       # 300 live < K
+    _custom("topk-big-values", 100000, 1, [], 100000, BIG, 5000, 1, strategies=(4,)),
+    _custom("topk-heavy-tail", 300000, 1, [], 300000, SPARSE, 16384, 1, strategies=(4,)),
+    _custom("topk-pareto-4M", 1 << 22, 1, [], 1 << 22, gen.PrioDist(gen.PRIO_PARETO, 1.5, float(1 << 24)), 8192, 1,
+            strategies=(4,)),
+]
+
+
+@pytest.mark.parametrize("w", TOPK_CASES, ids=[w.name for w in TOPK_CASES])
+def test_topk_matches_oracle(w):
+    p, next_seq = oracle_priorities(w)
+    t = gpu_table(w)
+    try:
+        for it in range(3):
+            say("%s iteration %d" % (w.name, it))
+            seed = gen.select_seed(w.seed, it)
+            idx, start, wt = t.select(gear.GEAR_TOPK, w.B, w.L, seed, 0.0, weights=True)
+            st, oidx, ostart, ow = oracle.select(oracle.TOPK, p, next_seq, w.T, w.B, w.L, seed, 0.0, True)
+            np.testing.assert_array_equal(host(idx), oidx)
+            np.testing.assert_array_equal(host(start), ostart)
+            np.testing.assert_array_equal(host(wt), ow)
+            assert t.sync() == (0 if st == oracle.OK else gear.GEAR_STATUS_NO_WEIGHT)
+            # New priorities for the selected slots change the next TopK.
+            sel = oidx[oidx >= 0]
+            newp = gen.update_priorities(w.prio, w.seed, it, sel.size) // 2
+            t.update_priorities(torch.from_numpy(sel).to(cuda()), torch.from_numpy(newp).to(cuda()))
+            oracle.update(p, sel, newp)
+    finally:
+        t.close()
+
+
+def test_topk_rejects_oversized_batch():
+    t = gear.Table([4], 10, 2)
+    try:
+        t.insert([np.zeros((10, 8), np.uint8)], np.ones(10, dtype=np.uint32))
+        with pytest.raises(gear.GearError) as e:
+            t.select(gear.GEAR_TOPK, gear.GEAR_MAX_TOPK + 1, 1, 0)
+        assert e.value.code == gear.GEAR_E_INVAL
+    finally:
+        t.close()
