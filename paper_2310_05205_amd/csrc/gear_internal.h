@@ -25,7 +25,10 @@ constexpr int kMaxLevels = 6;
 constexpr int kSearchMaxGrid = 2048;
 // TopK: at most this many workgroups per pass, and at most this many draws
 // (the final sort holds all K keys in one workgroup's LDS).
-constexpr int kTopkMaxGrid = 128;
+constexpr int kTopkMaxGrid = 256;
+constexpr int kTopkBins = 4096;       // bins of one TopK digit pass (12-bit digits)
+constexpr int kTopkStateWords = 8;
+constexpr int kTopkRankBlock = 512;    // keys one TopK rank workgroup compares against
 constexpr int kTopkMaxK = GEAR_MAX_TOPK;
 
 struct Table {
@@ -57,11 +60,11 @@ struct Table {
     uint32_t options = 0;             // GEAR_OPT_* bits
 
     // TopK scratch (fixed sizes).
-    uint32_t* topk_hist = nullptr;    // [3][2048] digit histograms, zero between calls
-    uint32_t* topk_state = nullptr;   // [3][4] per-pass selection state
-    uint32_t* topk_ticket = nullptr;  // [3] per-pass workgroup tickets, zero between calls
-    uint32_t* topk_counts = nullptr;  // [2][kTopkMaxGrid] per-workgroup counts above / at the threshold
-    uint64_t* topk_keys = nullptr;    // [kTopkMaxK] selected keys before sorting
+    uint32_t* topk_hist = nullptr;    // [3][kTopkBins] digit histograms, zero between calls
+    uint32_t* topk_state = nullptr;   // [kTopkStateWords] selection state after the digit passes
+    uint32_t* topk_local = nullptr;   // [3][kTopkMaxGrid][kTopkBins] per-workgroup suffix sums of each digit pass
+    uint64_t* topk_keys = nullptr;    // [kTopkMaxK] selected keys (p << 32 | ~slot), equal priorities in slot order
+    uint32_t* topk_rank = nullptr;    // [kTopkMaxK] place of each key in descending order
 };
 
 // Thread-local error reporting.

@@ -63,9 +63,9 @@ void free_table(Table* t) {
     (void)hipFree(t->wg_min);
     (void)hipFree(t->topk_hist);
     (void)hipFree(t->topk_state);
-    (void)hipFree(t->topk_ticket);
-    (void)hipFree(t->topk_counts);
+    (void)hipFree(t->topk_local);
     (void)hipFree(t->topk_keys);
+    (void)hipFree(t->topk_rank);
     (void)hipFree(t->status);
     delete t;
 }
@@ -174,11 +174,11 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
         }
     if ((e = dmalloc(&t->wg_min, sizeof(uint32_t) * gear::kSearchMaxGrid)) != hipSuccess) return oom("batch minima", e);
     if ((e = dmalloc(&t->status, sizeof(uint32_t))) != hipSuccess) return oom("status word", e);
-    if ((e = dmalloc(&t->topk_hist, sizeof(uint32_t) * 3 * 2048)) != hipSuccess ||
-        (e = dmalloc(&t->topk_state, sizeof(uint32_t) * 3 * 4)) != hipSuccess ||
-        (e = dmalloc(&t->topk_ticket, sizeof(uint32_t) * 3)) != hipSuccess ||
-        (e = dmalloc(&t->topk_counts, sizeof(uint32_t) * 2 * gear::kTopkMaxGrid)) != hipSuccess ||
-        (e = dmalloc(&t->topk_keys, sizeof(uint64_t) * gear::kTopkMaxK)) != hipSuccess)
+    if ((e = dmalloc(&t->topk_hist, sizeof(uint32_t) * 3 * gear::kTopkBins)) != hipSuccess ||
+        (e = dmalloc(&t->topk_state, sizeof(uint32_t) * gear::kTopkStateWords)) != hipSuccess ||
+        (e = dmalloc(&t->topk_local, sizeof(uint32_t) * 3 * gear::kTopkMaxGrid * gear::kTopkBins)) != hipSuccess ||
+        (e = dmalloc(&t->topk_keys, sizeof(uint64_t) * gear::kTopkMaxK)) != hipSuccess ||
+        (e = dmalloc(&t->topk_rank, sizeof(uint32_t) * gear::kTopkMaxK)) != hipSuccess)
         return oom("TopK scratch", e);
 
     if ((e = hipMemset(t->priority, 0, sizeof(uint32_t) * capacity)) != hipSuccess ||
@@ -186,9 +186,8 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
         (e = hipMemset(t->tile_sums, 0, sizeof(uint64_t) * t->ntiles)) != hipSuccess ||
         (e = hipMemset(t->wg_min, 0xFF, sizeof(uint32_t) * gear::kSearchMaxGrid)) != hipSuccess ||
         (e = hipMemset(t->status, 0, sizeof(uint32_t))) != hipSuccess ||
-        (e = hipMemset(t->topk_hist, 0, sizeof(uint32_t) * 3 * 2048)) != hipSuccess ||
-        (e = hipMemset(t->topk_state, 0, sizeof(uint32_t) * 3 * 4)) != hipSuccess ||
-        (e = hipMemset(t->topk_ticket, 0, sizeof(uint32_t) * 3)) != hipSuccess ||
+        (e = hipMemset(t->topk_hist, 0, sizeof(uint32_t) * 3 * gear::kTopkBins)) != hipSuccess ||
+        (e = hipMemset(t->topk_state, 0, sizeof(uint32_t) * gear::kTopkStateWords)) != hipSuccess ||
         (e = hipDeviceSynchronize()) != hipSuccess) {
         free_table(t);
         return hip_fail(e, "gear_table_create: initialising table state");

@@ -2,24 +2,41 @@
 // is deterministic; each GPU computes its top-K priority trajectories).
 //
 // The K highest priorities among slots with non-zero priority, higher
-// priority first, the lower slot first among equal priorities.  The K-th
-// largest priority P* is found by a radix select over the 32-bit priority in
-// three digit passes (bits 31..21, 20..10, 9..0):
+// priority first, the lower slot first among equal priorities.
 //
-//   topk_hist_kernel  (x3) a workgroup histograms one digit of the
-//                     priorities whose higher digits match the ones already
-//                     chosen; a wave whose lanes all fall into one bin adds
-//                     with a single LDS atomic (skewed priorities pile into
-//                     few bins).  The last workgroup to finish (one ticket
-//                     per workgroup) picks the bin that holds the K-th
-//                     largest, records how many of that bin are still to be
-//                     taken, and clears the histogram for the next call.
-//   topk_count_kernel per workgroup: how many priorities are > P* and == P*.
-//   topk_compact      every workgroup derives its output offsets from those
-//                     counts and writes keys (p << 32 | ~slot) of all slots
-//                     above P* and of the lowest-slot ties at P*.
-//   topk_sort_kernel  one workgroup sorts the K keys (bitonic, in LDS),
-//                     descending, and writes slots, window starts, weights.
+// The K-th largest priority is found by a radix select over a 36-bit key
+// that orders priorities like the priorities themselves: the position e of
+// the leading one (5 bits) above the e bits below it, left-aligned in 31
+// bits.  Its three 12-bit digits give small priorities their own pass-0
+// bins (every value below 256 is one bin) and spread skewed distributions
+// over many bins.  Selection stops early once the chosen bin is a single
+// value or is taken whole.  No workgroup waits for another and no kernel
+// fences memory: each kernel re-derives the digits chosen so far from the
+// complete histograms of the earlier passes, made visible by the kernel
+// boundary.
+//
+//   topk_hist_kernel    (x3) a workgroup histograms one digit of the keys
+//                       whose higher digits match the ones chosen so far,
+//                       in LDS (lanes of a wave that share a bin are peeled
+//                       off with one atomic for the whole group), adds its
+//                       bins into the pass's global histogram and stores the
+//                       suffix sums of its own histogram.
+//   topk_compact_kernel derives the threshold; the stored suffix sums give
+//                       every workgroup's count above and at it, hence this
+//                       workgroup's output offsets; one scan per batch of
+//                       loads orders its keys by slot.  It writes
+//                       (p << 32 | ~slot) of every slot above the threshold
+//                       and of the lowest-slot ones at it.
+//   topk_rank_kernel    a key's place in descending order is the number of
+//                       keys of higher priority plus those of equal priority
+//                       before it in the buffer (which is slot order); waves
+//                       count them over blocks of keys in parallel.
+//   topk_emit_kernel    writes slot, window start and weight at each key's
+//                       place, and clears the histograms for the next call.
+//
+// Loads that a derivation waits for are issued before the bulk priority
+// loads: vector loads complete in issue order, so the reverse would make the
+// derivation wait for the whole batch.
 #include "gear_internal.h"
 #include "wave.h"
 
@@ -28,19 +45,37 @@ namespace {
 
 constexpr int kTopkThreads = 1024;
 constexpr int kTopkWaves = kTopkThreads / 64;
+constexpr int kBins = kTopkBins;
+constexpr int kDigit = 12;
+constexpr int kKeyBits = 36;
+constexpr int kPasses = kKeyBits / kDigit;
+
+constexpr uint32_t kAll = 1u;           // fewer than K candidates: take every one
+constexpr uint32_t kDone = 2u;          // the threshold is fully determined
+constexpr uint32_t kInconsistent = 4u;  // histograms disagree (priorities changed mid-selection)
 
 struct TopkState {
-    uint32_t prefix;  // chosen high digits of the K-th largest priority
-    uint32_t k_rem;   // of the priorities matching `prefix`, how many are still to be taken
-    uint32_t all;     // 1: fewer than K slots have non-zero priority, take all of them
+    uint64_t prefix;  // key digits chosen so far
+    uint32_t k_rem;   // of the keys whose digits match `prefix`, how many are taken (lowest slots first)
     uint32_t total;   // number of slots with non-zero priority
+    int32_t passes;   // digits chosen; keys are compared after >> (36 - 12 * passes)
+    uint32_t flags;
 };
+static_assert(sizeof(TopkState) <= kTopkStateWords * sizeof(uint32_t), "state buffer");
 
-__device__ __forceinline__ int pass_shift(int pass) { return pass == 0 ? 21 : (pass == 1 ? 10 : 0); }
-__device__ __forceinline__ int pass_bits(int pass) { return pass == 2 ? 10 : 11; }
+// Order-preserving 36-bit key of a non-zero priority (0 maps to 0 like 1;
+// validity is tested separately).
+__device__ __forceinline__ uint64_t order_key(uint32_t p) {
+    const int e = 31 - __clz(p | 1u);
+    const uint32_t mant = (p << (31 - e)) & 0x7FFFFFFFu;
+    return ((uint64_t)e << 31) | mant;
+}
+
+__device__ __forceinline__ int state_shift(const TopkState& st) { return kKeyBits - kDigit * st.passes; }
+__device__ __forceinline__ bool decided(const TopkState& st) { return (st.flags & (kAll | kDone)) != 0; }
 
 // Slots [blockIdx.x * chunk, ...) of this workgroup; chunk is a multiple of
-// 4 so every 16-byte load is aligned.
+// 4 * kTopkThreads, so every 16-byte load is aligned.
 __device__ __forceinline__ void wg_range(int64_t N, int64_t chunk, int64_t& lo, int64_t& hi) {
     lo = (int64_t)blockIdx.x * chunk;
     hi = lo + chunk < N ? lo + chunk : N;
@@ -48,8 +83,9 @@ __device__ __forceinline__ void wg_range(int64_t N, int64_t chunk, int64_t& lo, 
 
 // One batch: kVec 16-byte loads per thread, all issued before any is used;
 // thread t, load k covers slots base + (k * kTopkThreads + t) * 4 .. +3,
-// and slots at or past `hi` read as priority 0 (never a candidate).
-constexpr int kVec = 8;
+// so (k, t, element) order is slot order.  Slots at or past `hi` read as
+// priority 0 (never a candidate).
+constexpr int kVec = 4;
 constexpr int64_t kBatch = (int64_t)kVec * kTopkThreads * 4;
 
 __device__ __forceinline__ void load_batch(const uint32_t* __restrict__ prio, int64_t base, int64_t hi,
@@ -67,200 +103,229 @@ __device__ __forceinline__ void load_batch(const uint32_t* __restrict__ prio, in
     }
 }
 
+// Thread t's four bins of a histogram row, kBins-4-4t .. kBins-1-4t (so
+// thread order is descending bin order; .w is the highest).
+__device__ __forceinline__ int first_bin() { return kBins - 4 - 4 * (int)threadIdx.x; }
+
+struct HistRows {
+    uint4 h[kPasses];
+};
+
+__device__ __forceinline__ void load_rows(const uint32_t* __restrict__ hist, int passes, HistRows& r) {
+#pragma unroll
+    for (int q = 0; q < kPasses; q++)
+        r.h[q] = q < passes ? *reinterpret_cast<const uint4*>(hist + q * kBins + first_bin()) : make_uint4(0, 0, 0, 0);
+}
+
+struct DeriveShared {
+    TopkState state[kPasses];
+    uint64_t wave_total[kPasses][kTopkWaves];
+};
+
+// Block-wide choice of digit pass q from its global histogram.
+__device__ TopkState derive_pass(uint4 h, int q, const TopkState& prev, uint32_t K, DeriveShared& sh) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const uint64_t part = (uint64_t)h.x + h.y + h.z + h.w;
+    const uint64_t incl = wave_inclusive_scan(part);
+    if (lane == 63) sh.wave_total[q][wave] = incl;
+    if (threadIdx.x == 0) {
+        TopkState f = prev;  // kept only if no bin holds the k_rem-th key
+        f.flags |= kDone | kInconsistent;
+        sh.state[q] = f;
+    }
+    __syncthreads();
+    uint64_t before = 0, total = 0;
+    for (int w = 0; w < kTopkWaves; w++) {
+        const uint64_t x = sh.wave_total[q][w];
+        before += w < wave ? x : 0;
+        total += x;
+    }
+    before += incl - part;
+    if (q == 0 && total < K) {
+        if (threadIdx.x == 0) {
+            TopkState st = prev;
+            st.total = (uint32_t)total;
+            st.flags = kAll;
+            sh.state[q] = st;
+        }
+    } else if (before < prev.k_rem && prev.k_rem <= before + part) {
+        const uint32_t bins[4] = {h.w, h.z, h.y, h.x};
+        const int top = first_bin() + 3;
+        uint64_t cum = before;
+        int j = 0;
+        while (j < 3 && cum + bins[j] < prev.k_rem) cum += bins[j++];
+        TopkState st = prev;
+        if (q == 0) st.total = (uint32_t)total;
+        st.prefix = (prev.prefix << kDigit) | (uint64_t)(top - j);
+        st.k_rem = prev.k_rem - (uint32_t)cum;
+        st.passes = q + 1;
+        const int mant_bits = kDigit * (q + 1) - 5;  // mantissa bits the prefix fixes
+        const int e = (int)(st.prefix >> mant_bits);
+        if (q + 1 == kPasses || bins[j] == st.k_rem || e <= mant_bits) st.flags |= kDone;
+        sh.state[q] = st;
+    }
+    __syncthreads();
+    return sh.state[q];
+}
+
+// State after at most `passes` digit passes of this call (fewer when an
+// earlier pass already decided).
+__device__ TopkState derive_rows(const HistRows& r, int passes, uint32_t K, DeriveShared& sh) {
+    TopkState st;
+    st.prefix = 0;
+    st.k_rem = K;
+    st.total = 0;
+    st.passes = 0;
+    st.flags = 0;
+#pragma unroll
+    for (int q = 0; q < kPasses; q++) {
+        if (q >= passes || decided(st)) break;
+        st = derive_pass(r.h[q], q, st, K, sh);
+    }
+    return st;
+}
+
 __global__ __launch_bounds__(kTopkThreads) void topk_hist_kernel(const uint32_t* __restrict__ prio, int64_t N,
                                                                  int64_t chunk, int pass, uint32_t K,
-                                                                 uint32_t* __restrict__ hist, TopkState* state,
-                                                                 uint32_t* ticket) {
-    __shared__ uint32_t sh[2048];
-    __shared__ int s_last;
-    const int nb = 1 << pass_bits(pass);
-    const int shift = pass_shift(pass);
-    TopkState prev;
-    if (pass == 0) {
-        prev.prefix = 0;
-        prev.k_rem = K;
-        prev.all = 0;
-        prev.total = 0;
-    } else {
-        prev = state[pass - 1];
-    }
-    if (prev.all) {  // nothing left to decide
-        if (blockIdx.x == 0 && threadIdx.x == 0) state[pass] = prev;
-        return;
-    }
-    const int prev_shift = pass == 0 ? 0 : pass_shift(pass - 1);
-    for (int b = threadIdx.x; b < nb; b += kTopkThreads) sh[b] = 0;
-    __syncthreads();
+                                                                 uint32_t* __restrict__ hist,
+                                                                 uint32_t* __restrict__ local) {
+    __shared__ __align__(16) uint32_t sh[kBins];
+    __shared__ DeriveShared dsh;
+    __shared__ uint64_t s_wt[kTopkWaves];
+    HistRows rows;
+    load_rows(hist, pass, rows);
+    const TopkState prev = derive_rows(rows, pass, K, dsh);
+    if (decided(prev)) return;  // nothing left to histogram
+    const int prev_shift = kKeyBits - kDigit * pass;
+    const int shift = prev_shift - kDigit;
     int64_t lo, hi;
     wg_range(N, chunk, lo, hi);
-    const int lane = threadIdx.x & 63;
+    uint32_t v[kVec][4];
+    load_batch(prio, lo, hi, v);
+    for (int b = threadIdx.x; b < kBins; b += kTopkThreads) sh[b] = 0;
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     for (int64_t base = lo; base < hi; base += kBatch) {
-        uint32_t v[kVec][4];
-        load_batch(prio, base, hi, v);
+        if (base != lo) load_batch(prio, base, hi, v);
 #pragma unroll
         for (int k = 0; k < kVec; k++) {
 #pragma unroll
             for (int q = 0; q < 4; q++) {
                 const uint32_t p = v[k][q];
-                const bool valid = p != 0u && (pass == 0 || (p >> prev_shift) == prev.prefix);
-                const uint32_t bin = (p >> shift) & (uint32_t)(nb - 1);
-                const unsigned long long vm = __ballot(valid);
-                if (vm == 0) continue;
-                const int first = __ffsll((long long)vm) - 1;
-                const uint32_t b0 = (uint32_t)__builtin_amdgcn_readlane((int)bin, first);
-                if (__ballot(valid && bin == b0) == vm) {
-                    if (lane == first) atomicAdd(&sh[b0], (uint32_t)__popcll(vm));
-                } else if (valid) {
-                    atomicAdd(&sh[bin], 1u);
+                const uint64_t key = order_key(p);
+                bool left = p != 0u && (pass == 0 || (key >> prev_shift) == prev.prefix);
+                const uint32_t bin = (uint32_t)(key >> shift) & (uint32_t)(kBins - 1);
+                uint64_t vm = __ballot(left);
+                for (int r = 0; r < 3 && vm != 0; r++) {
+                    const int first = __ffsll((long long)vm) - 1;
+                    const uint32_t b0 = (uint32_t)__builtin_amdgcn_readlane((int)bin, first);
+                    const uint64_t m = __ballot(left && bin == b0);
+                    if (lane == first) atomicAdd(&sh[b0], (uint32_t)__popcll(m));
+                    left = left && bin != b0;
+                    vm &= ~m;
+                    if (__popcll(m) < 4) break;
                 }
+                if (left) atomicAdd(&sh[bin], 1u);
             }
         }
     }
     __syncthreads();
-    for (int b = threadIdx.x; b < nb; b += kTopkThreads)
-        if (sh[b] != 0u) atomicAdd(&hist[b], sh[b]);
-    __threadfence();
+    // Add into the global histogram; store this workgroup's suffix sums
+    // (S[b] = its keys in bins >= b) for the offsets of the compaction.
+    const int b0 = first_bin();
+    const uint4 h = *reinterpret_cast<const uint4*>(&sh[b0]);
+    uint32_t* out = hist + pass * kBins + b0;
+    if (h.x) atomicAdd(out + 0, h.x);
+    if (h.y) atomicAdd(out + 1, h.y);
+    if (h.z) atomicAdd(out + 2, h.z);
+    if (h.w) atomicAdd(out + 3, h.w);
+    const uint64_t part = (uint64_t)h.x + h.y + h.z + h.w;
+    const uint64_t incl = wave_inclusive_scan(part);
+    if (lane == 63) s_wt[wave] = incl;
     __syncthreads();
-    if (threadIdx.x == 0) s_last = atomicAdd(ticket, 1u) == gridDim.x - 1;
-    __syncthreads();
-    if (!s_last) return;
-
-    // The last workgroup: every other workgroup's histogram is in.
-    __threadfence();
-    for (int b = threadIdx.x; b < nb; b += kTopkThreads)
-        sh[b] = __hip_atomic_load(&hist[b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __syncthreads();
-    if (threadIdx.x < 64) {
-        // Lane l covers bins top, top-1, .., top-per+1 (the highest bins in lane 0).
-        const int per = nb / 64;
-        const int top = nb - 1 - lane * per;
-        uint64_t part = 0;
-        for (int k = 0; k < per; k++) part += sh[top - k];
-        const uint64_t incl = wave_inclusive_scan(part);
-        const uint64_t total = read_lane(incl, 63);
-        TopkState st = prev;
-        if (pass == 0) st.total = (uint32_t)total;
-        if (pass == 0 && total < K) {
-            st.all = 1;
-            if (lane == 0) state[pass] = st;
-        } else {
-            // The sub-histogram holds at least k_rem entries (the chosen bin of
-            // the previous pass did), so some lane reaches k_rem.
-            const int L = __ffsll((long long)__ballot(incl >= prev.k_rem)) - 1;
-            if (lane == L) {
-                uint64_t cum = incl - part;
-                int sel = top - per + 1;
-                for (int k = 0; k < per; k++) {
-                    const int b = top - k;
-                    if (cum + sh[b] >= prev.k_rem) {
-                        sel = b;
-                        break;
-                    }
-                    cum += sh[b];
-                }
-                st.prefix = (prev.prefix << pass_bits(pass)) | (uint32_t)sel;
-                st.k_rem = prev.k_rem - (uint32_t)cum;
-                state[pass] = st;
-            }
-        }
-    }
-    __syncthreads();
-    for (int b = threadIdx.x; b < nb; b += kTopkThreads) hist[b] = 0u;  // ready for the next call
-    if (threadIdx.x == 0) *ticket = 0u;
+    uint64_t above = incl - part;
+    for (int w = 0; w < wave; w++) above += s_wt[w];
+    uint4 S;
+    S.w = (uint32_t)(above + h.w);
+    S.z = S.w + h.z;
+    S.y = S.z + h.y;
+    S.x = S.y + h.x;
+    *reinterpret_cast<uint4*>(local + ((size_t)pass * kTopkMaxGrid + blockIdx.x) * kBins + b0) = S;
 }
 
-__device__ __forceinline__ void classify(uint32_t p, const TopkState& st, bool& gt, bool& eq) {
-    if (st.all) {
+// Above / at the threshold of a decided state.
+__device__ __forceinline__ void classify(uint32_t p, const TopkState& st, int shift, bool& gt, bool& eq) {
+    if (st.flags & kAll) {
         gt = p != 0u;
         eq = false;
     } else {
-        gt = p > st.prefix;
-        eq = p == st.prefix;
+        const uint64_t k = order_key(p) >> shift;
+        gt = p != 0u && k > st.prefix;
+        eq = p != 0u && k == st.prefix;
     }
 }
 
-__global__ __launch_bounds__(kTopkThreads) void topk_count_kernel(const uint32_t* __restrict__ prio, int64_t N,
-                                                                  int64_t chunk, const TopkState* state,
-                                                                  uint32_t* __restrict__ counts, int grid) {
-    __shared__ uint64_t s_gt[kTopkWaves], s_eq[kTopkWaves];
-    const TopkState st = state[2];
-    int64_t lo, hi;
-    wg_range(N, chunk, lo, hi);
-    uint32_t ngt = 0, neq = 0;
-    for (int64_t base = lo; base < hi; base += kBatch) {
-        uint32_t v[kVec][4];
-        load_batch(prio, base, hi, v);
-#pragma unroll
-        for (int k = 0; k < kVec; k++)
-#pragma unroll
-            for (int q = 0; q < 4; q++) {
-                bool gt, eq;
-                classify(v[k][q], st, gt, eq);
-                ngt += gt;
-                neq += eq;
-            }
+// Workgroup g's keys above and at the threshold, from its suffix sums of
+// every pass that ran.
+__device__ __forceinline__ void wg_counts(const uint32_t* __restrict__ local, const TopkState& st, int g,
+                                          uint32_t& gt, uint32_t& eq) {
+    if (st.flags & kAll) {
+        gt = local[(size_t)g * kBins];  // pass 0 counted every non-zero priority
+        eq = 0;
+        return;
     }
-    const uint64_t wgt = wave_sum(ngt), weq = wave_sum(neq);
-    if ((threadIdx.x & 63) == 0) {
-        s_gt[threadIdx.x >> 6] = wgt;
-        s_eq[threadIdx.x >> 6] = weq;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint64_t a = 0, b = 0;
-        for (int k = 0; k < kTopkWaves; k++) {
-            a += s_gt[k];
-            b += s_eq[k];
-        }
-        counts[blockIdx.x] = (uint32_t)a;
-        counts[grid + blockIdx.x] = (uint32_t)b;
-    }
-}
-
-// Thread t of a workgroup owns the contiguous run of `run` slots starting
-// at lo + t * run (run = chunk / kTopkThreads, a multiple of 4), so slot
-// order is thread order and one block-wide scan of per-thread counts gives
-// every output position.
-__device__ __forceinline__ void count_run(const uint32_t* __restrict__ prio, int64_t r0, int64_t r1,
-                                          const TopkState& st, uint32_t& ngt, uint32_t& neq) {
-    ngt = 0;
-    neq = 0;
-    for (int64_t e = r0; e < r1; e += 4) {
-        uint32_t v[4];
-        if (e + 4 <= r1) {
-            const uint4 x = *reinterpret_cast<const uint4*>(prio + e);
-            v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
-        } else {
+    gt = 0;
+    eq = 0;
 #pragma unroll
-            for (int q = 0; q < 4; q++) v[q] = e + q < r1 ? prio[e + q] : 0u;
-        }
-#pragma unroll
-        for (int q = 0; q < 4; q++) {
-            bool gt, eq;
-            classify(v[q], st, gt, eq);
-            ngt += gt;
-            neq += eq;
-        }
+    for (int q = 0; q < kPasses; q++) {
+        if (q >= st.passes) break;
+        const uint32_t* row = local + ((size_t)q * kTopkMaxGrid + g) * kBins;
+        const int sel = (int)(st.prefix >> (kDigit * (st.passes - 1 - q))) & (kBins - 1);
+        const uint32_t above = sel + 1 < kBins ? row[sel + 1] : 0u;
+        gt += above;
+        if (q == st.passes - 1) eq = row[sel] - above;
     }
 }
 
 __global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(const uint32_t* __restrict__ prio, int64_t N,
-                                                                    int64_t chunk, const TopkState* state,
-                                                                    const uint32_t* __restrict__ counts, int grid,
-                                                                    uint64_t* __restrict__ keys) {
-    __shared__ uint64_t s_wgt[kTopkWaves], s_weq[kTopkWaves];
-    __shared__ uint64_t s_base[3];  // gt base, eq base, total above P*
-    const TopkState st = state[2];
+                                                                    int64_t chunk, uint32_t K,
+                                                                    const uint32_t* __restrict__ hist,
+                                                                    const uint32_t* __restrict__ local, int grid,
+                                                                    TopkState* state,
+                                                                    uint64_t* __restrict__ keys,
+                                                                    uint32_t* __restrict__ rank) {
+    __shared__ DeriveShared dsh;
+    __shared__ uint64_t s_pre[kVec * kTopkWaves];  // per (load, wave): packed counts, then their prefix
+    __shared__ uint64_t s_base[5];                 // above base, at base, total above, own above, own at
+    __shared__ uint64_t s_batch;                   // packed counts of the whole batch
+    HistRows rows;
+    load_rows(hist, kPasses, rows);
+    int64_t lo, hi;
+    wg_range(N, chunk, lo, hi);
+    uint32_t v[kVec][4];
+    load_batch(prio, lo, hi, v);
+    const TopkState st = derive_rows(rows, kPasses, K, dsh);
+    if (blockIdx.x == 0 && threadIdx.x == 0) *state = st;
+    // The rank kernel accumulates into rank: start it at zero.
+    for (int k = blockIdx.x * kTopkThreads + threadIdx.x; k < (int)K; k += grid * kTopkThreads) rank[k] = 0u;
+    const int shift = state_shift(st);
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     if (wave == 0) {
         uint64_t gb = 0, eb = 0, tot = 0;
-        for (int w = lane; w < grid; w += 64) {
-            const uint64_t g = counts[w], e = counts[grid + w];
-            tot += g;
-            if (w < (int)blockIdx.x) {
-                gb += g;
-                eb += e;
+#pragma unroll
+        for (int r = 0; r < kTopkMaxGrid / 64; r++) {
+            const int g = lane + 64 * r;
+            uint32_t gt = 0, eq = 0;
+            if (g < grid) wg_counts(local, st, g, gt, eq);
+            tot += gt;
+            if (g < (int)blockIdx.x) {
+                gb += gt;
+                eb += eq;
+            }
+            if (g == (int)blockIdx.x) {
+                s_base[3] = gt;
+                s_base[4] = eq;
             }
         }
         gb = wave_sum(gb);
@@ -272,149 +337,160 @@ __global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(const uint32
             s_base[2] = tot;
         }
     }
-    int64_t lo, hi;
-    wg_range(N, chunk, lo, hi);
-    const int64_t run = chunk / kTopkThreads;
-    int64_t r0 = lo + (int64_t)threadIdx.x * run;
-    int64_t r1 = r0 + run;
-    if (r0 > hi) r0 = hi;
-    if (r1 > hi) r1 = hi;
-    uint32_t ngt, neq;
-    count_run(prio, r0, r1, st, ngt, neq);
-    // Exclusive prefix of the per-thread counts across the workgroup.
-    const uint64_t ig = wave_inclusive_scan(ngt), ie = wave_inclusive_scan(neq);
-    if (lane == 63) {
-        s_wgt[wave] = ig;
-        s_weq[wave] = ie;
-    }
     __syncthreads();
-    uint64_t pg = 0, pe = 0;
-    for (int k = 0; k < wave; k++) {
-        pg += s_wgt[k];
-        pe += s_weq[k];
-    }
-    uint64_t og = s_base[0] + pg + ig - ngt;  // output position of this thread's first slot above P*
-    uint64_t oe = s_base[1] + pe + ie - neq;  // rank of its first tie among all ties, in slot order
+    const uint64_t e_need = (st.flags & kAll) ? 0 : st.k_rem;
     const uint64_t total_gt = s_base[2];
-    const uint64_t e_need = st.all ? 0 : st.k_rem;
-    if (ngt == 0 && (neq == 0 || oe >= e_need)) return;
-    for (int64_t e0 = r0; e0 < r1; e0 += 4 * kVec) {
-        // Reload the run kVec x 4 slots at a time, all loads in flight together.
-        uint32_t v[kVec][4];
+    uint64_t run_gt = s_base[0], run_eq = s_base[1];
+    if (s_base[3] == 0 && (s_base[4] == 0 || run_eq >= e_need)) return;
+    for (int64_t base = lo; base < hi; base += kBatch) {
+        if (base != lo) load_batch(prio, base, hi, v);
+        uint64_t c[kVec], incl[kVec];
+        uint32_t cls[kVec];  // per element: bit q above, bit 4 + q at
 #pragma unroll
         for (int k = 0; k < kVec; k++) {
-            const int64_t e = e0 + 4 * k;
-            if (e + 4 <= r1) {
-                const uint4 x = *reinterpret_cast<const uint4*>(prio + e);
-                v[k][0] = x.x; v[k][1] = x.y; v[k][2] = x.z; v[k][3] = x.w;
-            } else {
-#pragma unroll
-                for (int q = 0; q < 4; q++) v[k][q] = e + q < r1 ? prio[e + q] : 0u;
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < kVec; k++)
+            c[k] = 0;
+            cls[k] = 0;
 #pragma unroll
             for (int q = 0; q < 4; q++) {
-                const int64_t e = e0 + 4 * k + q;
-                if (e >= r1) continue;
-                const uint32_t p = v[k][q];
                 bool gt, eq;
-                classify(p, st, gt, eq);
-                const uint64_t key = ((uint64_t)p << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)e);
-                if (gt) keys[og++] = key;
-                if (eq) {
-                    if (oe < e_need) keys[total_gt + oe] = key;
+                classify(v[k][q], st, shift, gt, eq);
+                c[k] += (uint64_t)gt | ((uint64_t)eq << 32);
+                cls[k] |= (gt ? 1u << q : 0u) | (eq ? 16u << q : 0u);
+            }
+            incl[k] = wave_inclusive_scan(c[k]);
+            if (lane == 63) s_pre[k * kTopkWaves + wave] = incl[k];
+        }
+        __syncthreads();
+        if (wave == 0) {
+            // Exclusive scan of the kVec x kTopkWaves wave counts in (load, wave) order.
+            const uint64_t a = s_pre[lane];
+            const uint64_t s = wave_inclusive_scan(a);
+            s_pre[lane] = s - a;
+            if (lane == 63) s_batch = s;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < kVec; k++) {
+            if (cls[k] == 0) continue;
+            const uint64_t off = s_pre[k * kTopkWaves + wave] + incl[k] - c[k];
+            uint64_t og = run_gt + (uint32_t)off;  // output position of this lane's first key above
+            uint64_t oe = run_eq + (off >> 32);    // slot-order rank of its first key at the threshold
+            const int64_t e0 = base + ((int64_t)k * kTopkThreads + threadIdx.x) * 4;
+#pragma unroll
+            for (int q = 0; q < 4; q++) {
+                const uint64_t key = ((uint64_t)v[k][q] << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)(e0 + q));
+                // The counts bound both positions by K; the checks keep a
+                // priority changed under a running selection from writing
+                // past the key buffer.
+                if (cls[k] & (1u << q)) {
+                    if (og < (uint64_t)K) keys[og] = key;
+                    og++;
+                }
+                if (cls[k] & (16u << q)) {
+                    if (oe < e_need && total_gt + oe < (uint64_t)K) keys[total_gt + oe] = key;
                     oe++;
                 }
             }
+        }
+        const uint64_t tb = s_batch;
+        run_gt += (uint32_t)tb;
+        run_eq += tb >> 32;
+        __syncthreads();  // s_pre and s_batch are rewritten by the next batch
     }
 }
+static_assert(kVec * kTopkWaves == 64, "one lane of wave 0 per (load, wave) count");
 
-__global__ __launch_bounds__(kTopkThreads) void topk_sort_kernel(const uint64_t* __restrict__ keys,
-                                                                 const TopkState* state, int32_t K, uint64_t span,
-                                                                 uint64_t seed, int64_t* __restrict__ idx,
-                                                                 int32_t* __restrict__ start, float* __restrict__ w,
-                                                                 uint32_t* status) {
-    __shared__ uint64_t sk[kTopkMaxK];
-    const TopkState st = state[2];
-    const int n = st.all ? (int)st.total : K;  // keys written by the compaction
-    int npow = 1;
-    while (npow < n) npow <<= 1;
-    for (int k = threadIdx.x; k < npow; k += kTopkThreads) sk[k] = k < n ? keys[k] : 0ull;
+// Number of selected keys: K, or every candidate when there are fewer.
+__device__ __forceinline__ int selected(const TopkState& st, int32_t K) {
+    return (st.flags & kAll) ? (int)st.total : K;
+}
+
+// Keys are unique (they hold the slot), so key i's place in descending
+// order is the number of larger keys.  blockIdx.x: 256 keys, one per thread;
+// blockIdx.y: a block of kRankBlock keys staged in LDS, read two at a time
+// with all lanes on the same address; the counts of all blocks are added
+// into rank[i].
+constexpr int kRankKeys = 256;
+constexpr int kRankBlock = kTopkRankBlock;
+
+__global__ __launch_bounds__(kRankKeys) void topk_rank_kernel(const uint64_t* __restrict__ keys,
+                                                              const TopkState* __restrict__ state, int32_t K,
+                                                              uint32_t* __restrict__ rank) {
+    __shared__ ulonglong2 blk[kRankBlock / 2];
+    const int n = selected(*state, K);
+    const int i0 = blockIdx.x * kRankKeys;
+    const int j0 = blockIdx.y * kRankBlock;
+    if (i0 >= n || j0 >= n) return;
+    uint64_t* b64 = reinterpret_cast<uint64_t*>(blk);
+    for (int jj = threadIdx.x; jj < kRankBlock; jj += kRankKeys)
+        b64[jj] = j0 + jj < n ? keys[j0 + jj] : 0ull;  // 0: below every key (p >= 1)
+    const int i = i0 + (int)threadIdx.x;
+    const uint64_t mine = i < n ? keys[i] : ~0ull;
     __syncthreads();
-    // Bitonic sort, descending: a key is (priority << 32) | ~slot, so larger
-    // keys are higher priorities and, among equal priorities, lower slots.
-    constexpr int kPairs = kTopkMaxK / 2 / kTopkThreads;  // pairs per thread at the largest size
-    for (int k = 2; k <= npow; k <<= 1) {
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            // The pairs of one step are disjoint: load them all, then compare,
-            // then store, so each step costs one LDS round trip.
-            uint64_t x[kPairs], y[kPairs];
-            int a[kPairs];
-#pragma unroll
-            for (int r = 0; r < kPairs; r++) {
-                const int t = threadIdx.x + r * kTopkThreads;
-                a[r] = -1;
-                if (t < (npow >> 1)) {
-                    a[r] = ((t & ~(j - 1)) << 1) | (t & (j - 1));
-                    x[r] = sk[a[r]];
-                    y[r] = sk[a[r] | j];
-                }
-            }
-#pragma unroll
-            for (int r = 0; r < kPairs; r++) {
-                if (a[r] < 0) continue;
-                const bool down = (a[r] & k) == 0;
-                if (down ? (x[r] < y[r]) : (x[r] > y[r])) {
-                    sk[a[r]] = y[r];
-                    sk[a[r] | j] = x[r];
-                }
-            }
-            __syncthreads();
-        }
+    uint32_t c0 = 0, c1 = 0;
+#pragma unroll 16
+    for (int q = 0; q < kRankBlock / 2; q++) {
+        const ulonglong2 y = blk[q];
+        c0 += y.x > mine;
+        c1 += y.y > mine;
     }
-    for (int b = threadIdx.x; b < K; b += kTopkThreads) {
-        if (b < n) {
-            idx[b] = (int64_t)(0xFFFFFFFFu - (uint32_t)sk[b]);
-            start[b] = (int32_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b + 1), span);
-            if (w) w[b] = 1.0f;
-        } else {
-            idx[b] = -1;
-            start[b] = 0;
-            if (w) w[b] = 0.0f;
+    if (i < n && c0 + c1) atomicAdd(&rank[i], c0 + c1);
+}
+
+__global__ void topk_emit_kernel(const uint64_t* __restrict__ keys, const uint32_t* __restrict__ rank,
+                                 const TopkState* __restrict__ state, int32_t K, uint64_t span, uint64_t seed,
+                                 int64_t* __restrict__ idx, int32_t* __restrict__ start, float* __restrict__ w,
+                                 uint32_t* status, uint32_t* __restrict__ hist) {
+    const TopkState st = *state;
+    const int n = selected(st, K);
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t < kPasses * kBins) hist[t] = 0u;  // every digit pass of this call is done
+    if (t == 0 && (st.flags & kInconsistent)) atomicOr(status, GEAR_STATUS_INTERNAL);
+    if (t >= K) return;
+    if (t < n) {
+        const uint32_t b = rank[t];  // a permutation of 0 .. n-1
+        if (b >= (uint32_t)n) {
+            atomicOr(status, GEAR_STATUS_INTERNAL);
+            return;
         }
+        idx[b] = (int64_t)(0xFFFFFFFFu - (uint32_t)keys[t]);
+        start[b] = (int32_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b + 1), span);
+        if (w) w[b] = 1.0f;
+    } else {
+        idx[t] = -1;
+        start[t] = 0;
+        if (w) w[t] = 0.0f;
+        if (t == n) atomicOr(status, GEAR_STATUS_NO_WEIGHT);
     }
-    if (threadIdx.x == 0 && n < K) atomicOr(status, GEAR_STATUS_NO_WEIGHT);
 }
 
 }  // namespace
 
 hipError_t launch_topk(Table& t, int32_t K, int32_t L, uint64_t seed, int64_t* idx, int32_t* start, float* w,
                        hipStream_t s) {
-    // chunk: a multiple of 4 * kTopkThreads (aligned loads, whole per-thread runs).
-    const int64_t unit = 4 * 1024;
+    // chunk: a multiple of 4 * kTopkThreads (aligned 16-byte loads).
+    const int64_t unit = 4 * kTopkThreads;
     int64_t g = (t.N + unit - 1) / unit;
     g = g < kTopkMaxGrid ? g : kTopkMaxGrid;
     const int64_t chunk = ((t.N + g - 1) / g + unit - 1) / unit * unit;
     const int grid = (int)((t.N + chunk - 1) / chunk);
     TopkState* state = reinterpret_cast<TopkState*>(t.topk_state);
-    for (int pass = 0; pass < 3; pass++) {
+    hipError_t e;
+    for (int pass = 0; pass < kPasses; pass++) {
         hipLaunchKernelGGL(topk_hist_kernel, dim3(grid), dim3(kTopkThreads), 0, s, t.priority, t.N, chunk, pass,
-                           (uint32_t)K, t.topk_hist + pass * 2048, state, t.topk_ticket + pass);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
+                           (uint32_t)K, t.topk_hist, t.topk_local);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(topk_count_kernel, dim3(grid), dim3(kTopkThreads), 0, s, t.priority, t.N, chunk, state,
-                       t.topk_counts, grid);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(topk_compact_kernel, dim3(grid), dim3(kTopkThreads), 0, s, t.priority, t.N, chunk, state,
-                       t.topk_counts, grid, t.topk_keys);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(topk_sort_kernel, dim3(1), dim3(kTopkThreads), 0, s, t.topk_keys, state, K,
-                       (uint64_t)(t.T - L + 1), seed, idx, start, w, t.status);
+    hipLaunchKernelGGL(topk_compact_kernel, dim3(grid), dim3(kTopkThreads), 0, s, t.priority, t.N, chunk,
+                       (uint32_t)K, t.topk_hist, t.topk_local, grid, state, t.topk_keys, t.topk_rank);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(topk_rank_kernel, dim3((K + kRankKeys - 1) / kRankKeys, (K + kRankBlock - 1) / kRankBlock),
+                       dim3(kRankKeys), 0, s,
+                       t.topk_keys, state, K, t.topk_rank);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const int emit = K > kPasses * kBins ? K : kPasses * kBins;
+    hipLaunchKernelGGL(topk_emit_kernel, dim3((emit + 255) / 256), dim3(256), 0, s, t.topk_keys, t.topk_rank, state,
+                       K, (uint64_t)(t.T - L + 1), seed, idx, start, w, t.status, t.topk_hist);
     return hipGetLastError();
 }
 

@@ -382,6 +382,12 @@ TOPK_CASES = [
     _custom("topk-heavy-tail", 300000, 1, [], 300000, SPARSE, 16384, 1, strategies=(4,)),
     _custom("topk-pareto-4M", 1 << 22, 1, [], 1 << 22, gen.PrioDist(gen.PRIO_PARETO, 1.5, float(1 << 24)), 8192, 1,
             strategies=(4,)),
+    # 4096 large values sharing their top 24 key bits: all three digit passes run.
+    _custom("topk-three-pass", 100000, 1, [], 100000, gen.PrioDist(gen.PRIO_UNIFORM, 0x80000000, 0x80000FFF), 5000, 1,
+            strategies=(4,)),
+    # Several batches per workgroup with a ragged tail, and the largest K.
+    _custom("topk-multi-batch-maxK", (1 << 23) + 12345, 1, [], (1 << 23) + 12345,
+            gen.PrioDist(gen.PRIO_LOGNORMAL, 6.931471805599453, 1.0, float(1 << 24)), 16384, 1, strategies=(4,)),
 ]
 
 
