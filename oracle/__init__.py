@@ -33,6 +33,17 @@ def build(force=False):
     return _LIB
 
 
+class _Im(ctypes.Structure):
+    """Mirror of the oracle's index-manager struct (orc_im)."""
+    _fields_ = [("N", ctypes.c_int64), ("removal", ctypes.c_int), ("max_sel", ctypes.c_int64),
+                ("free_q", ctypes.POINTER(ctypes.c_int64)), ("n_free", ctypes.c_int64),
+                ("committed", ctypes.POINTER(ctypes.c_int64)), ("n_committed", ctypes.c_int64),
+                ("n_pending", ctypes.c_int64), ("state", ctypes.POINTER(ctypes.c_uint8))]
+
+
+IM_FREE, IM_PENDING, IM_COMMITTED = 0, 1, 2
+_NO_ORDER = np.zeros(1, dtype=np.int64)
+
 _lib = None
 
 
@@ -48,7 +59,7 @@ def lib():
         L.oracle_bounded.argtypes = [u64, u64]; L.oracle_bounded.restype = u64
         L.oracle_prefix_sum.argtypes = [vp, i64, vp]; L.oracle_prefix_sum.restype = u64
         L.oracle_upper_bound.argtypes = [vp, i64, u64]; L.oracle_upper_bound.restype = i64
-        L.oracle_select.argtypes = [ctypes.c_int, vp, i64, u64, i32, i32, i32, u64, ctypes.c_float,
+        L.oracle_select.argtypes = [ctypes.c_int, vp, i64, u64, vp, i64, i32, i32, i32, u64, ctypes.c_float,
                                     vp, vp, vp, vp]
         L.oracle_select.restype = ctypes.c_int
         L.oracle_collect.argtypes = [i32, vp, vp, i64, i32, vp, vp, i32, i32, vp]
@@ -58,6 +69,12 @@ def lib():
         L.oracle_insert.restype = u64
         L.oracle_translate.argtypes = [i64, i64, vp, vp]
         L.oracle_translate.restype = ctypes.c_int
+        imp = ctypes.POINTER(_Im)
+        L.oracle_im_init.argtypes = [imp, i64, ctypes.c_int, i64]; L.oracle_im_init.restype = ctypes.c_int
+        L.oracle_im_free.argtypes = [imp]; L.oracle_im_free.restype = None
+        L.oracle_im_allocate.argtypes = [imp, i64, vp, vp]; L.oracle_im_allocate.restype = ctypes.c_int
+        L.oracle_im_commit.argtypes = [imp, i64, vp, vp, vp]; L.oracle_im_commit.restype = ctypes.c_int
+        L.oracle_im_update.argtypes = [imp, vp, vp, vp, i32]; L.oracle_im_update.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -93,15 +110,23 @@ def upper_bound(C, r):
     return lib().oracle_upper_bound(_ptr(C), C.size, r)
 
 
-def select(strategy, priority, next_seq, T, B, L, seed, beta=0.0, weights=False):
-    """Returns (status, idx int64[B], start int32[B], w float32[B] or None)."""
+def select(strategy, priority, next_seq, T, B, L, seed, beta=0.0, weights=False, order=None):
+    """Returns (status, idx int64[B], start int32[B], w float32[B] or None).
+    `order`: the committed slots of an index manager, oldest first (FIFO,
+    LIFO and uniform pick from it); None for the ring state `next_seq`."""
     priority = np.ascontiguousarray(priority, dtype=np.uint32)
     N = priority.size
     idx = np.zeros(max(B, 0), dtype=np.int64)
     start = np.zeros(max(B, 0), dtype=np.int32)
     w = np.zeros(max(B, 0), dtype=np.float32) if weights else None
     C = np.empty(N, dtype=np.uint64) if strategy == PRIORITIZED else None
-    st = lib().oracle_select(strategy, _ptr(priority), N, next_seq, T, B, L, seed,
+    if order is not None:
+        order = np.ascontiguousarray(order, dtype=np.int64)
+        # A non-NULL pointer even for an empty list (never read then).
+        optr, nord = (_ptr(order) if order.size else _ptr(_NO_ORDER)), order.size
+    else:
+        optr, nord = None, 0
+    st = lib().oracle_select(strategy, _ptr(priority), N, next_seq, optr, nord, T, B, L, seed,
                              ctypes.c_float(beta), _ptr(idx), _ptr(start), _ptr(w), _ptr(C))
     return st, idx, start, w
 
@@ -140,9 +165,68 @@ def translate(global_idx, capacity):
     return s.value, l.value
 
 
+class IndexManager:
+    """The oracle's index manager: a free-index queue, a per-index state and
+    the committed indices in commit order, with FIFO or LIFO removal and a
+    maximum of selectable indices (oracle_im_* in oracle.c)."""
+
+    def __init__(self, N, removal, max_sel):
+        self._m = _Im()
+        st = lib().oracle_im_init(ctypes.byref(self._m), int(N), int(removal), int(max_sel))
+        if st != OK:
+            raise ValueError("invalid index-manager parameters")
+
+    def __del__(self):
+        if getattr(self, "_m", None) is not None and lib is not None:
+            lib().oracle_im_free(ctypes.byref(self._m))
+            self._m = None
+
+    @property
+    def n_committed(self):
+        return self._m.n_committed
+
+    @property
+    def n_pending(self):
+        return self._m.n_pending
+
+    @property
+    def n_free(self):
+        return self._m.n_free
+
+    def order(self):
+        """Committed indices, oldest commit first (a copy)."""
+        return np.ctypeslib.as_array(self._m.committed, shape=(self._m.N,))[:self._m.n_committed].copy()
+
+    def free_queue(self):
+        return np.ctypeslib.as_array(self._m.free_q, shape=(self._m.N,))[:self._m.n_free].copy()
+
+    def state(self):
+        return np.ctypeslib.as_array(self._m.state, shape=(self._m.N,)).copy()
+
+    def allocate(self, n, priority):
+        """Returns (status, idx int64[n]); victims' priorities are zeroed."""
+        assert priority.dtype == np.uint32 and priority.flags.c_contiguous
+        idx = np.zeros(max(int(n), 1), dtype=np.int64)
+        st = lib().oracle_im_allocate(ctypes.byref(self._m), int(n), _ptr(idx), _ptr(priority))
+        return st, idx[:int(n)]
+
+    def commit(self, idx, prio, priority):
+        assert priority.dtype == np.uint32 and priority.flags.c_contiguous
+        idx = np.ascontiguousarray(idx, dtype=np.int64)
+        prio = np.ascontiguousarray(prio, dtype=np.uint32)
+        return lib().oracle_im_commit(ctypes.byref(self._m), idx.size, _ptr(idx), _ptr(prio), _ptr(priority))
+
+    def update(self, priority, idx, newp):
+        assert priority.dtype == np.uint32 and priority.flags.c_contiguous
+        idx = np.ascontiguousarray(idx, dtype=np.int64)
+        newp = np.ascontiguousarray(newp, dtype=np.uint32)
+        return lib().oracle_im_update(ctypes.byref(self._m), _ptr(priority), _ptr(idx), _ptr(newp), idx.size)
+
+
 class Store:
     """Host-memory store driven through the oracle: columns [N, T*E_c] bytes,
-    priorities uint32[N] and the insertion count."""
+    priorities uint32[N] and the insertion count; optionally managed by an
+    IndexManager (use_allocator) instead of the ring."""
 
     def __init__(self, elem_bytes, N, T):
         self.E = [int(e) for e in elem_bytes]
@@ -150,12 +234,37 @@ class Store:
         self.cols = [np.zeros((self.N, self.T * e), dtype=np.uint8) for e in self.E]
         self.priority = np.zeros(self.N, dtype=np.uint32)
         self.next_seq = 0
+        self.im = None
+
+    def use_allocator(self, removal, max_sel):
+        assert self.next_seq == 0 and self.im is None
+        self.im = IndexManager(self.N, removal, max_sel)
+
+    def allocate(self, n):
+        return self.im.allocate(n, self.priority)
+
+    def write(self, idx, rows):
+        """Writes rows[c][r] into block idx[r] of column c (in place)."""
+        for c, r in enumerate(rows):
+            self.cols[c][np.asarray(idx, dtype=np.int64)] = np.ascontiguousarray(r).reshape(len(idx), -1).view(np.uint8)
+
+    def commit(self, idx, prio):
+        return self.im.commit(idx, prio, self.priority)
 
     def insert(self, rows, prio):
-        """rows: list (per column) of uint8 arrays [n, T*E_c]; prio uint32[n]."""
+        """rows: list (per column) of uint8 arrays [n, T*E_c]; prio uint32[n].
+        With an index manager: one allocate of n, the writes, one commit."""
         n = int(np.asarray(prio).size)
         rows = [np.ascontiguousarray(r).reshape(n, -1).view(np.uint8) for r in rows]
         prio = np.ascontiguousarray(prio, dtype=np.uint32)
+        if self.im is not None:
+            st, idx = self.allocate(n)
+            if st != OK:
+                return st
+            self.write(idx, rows)
+            st = self.commit(idx, prio)
+            self.next_seq += n
+            return st
         Ea = np.array(self.E, dtype=np.int64)
         bases = (ctypes.c_void_p * len(self.cols))(*[c.ctypes.data for c in self.cols])
         srcs = (ctypes.c_void_p * len(rows))(*[r.ctypes.data for r in rows])
@@ -163,11 +272,14 @@ class Store:
                                             self.next_seq, n, srcs, _ptr(self.priority), _ptr(prio))
 
     def select(self, strategy, B, L, seed, beta=0.0, weights=False):
-        return select(strategy, self.priority, self.next_seq, self.T, B, L, seed, beta, weights)
+        order = self.im.order() if self.im is not None else None
+        return select(strategy, self.priority, self.next_seq, self.T, B, L, seed, beta, weights, order)
 
     def collect(self, idx, start, L, col_ids=None):
         cols = self.cols if col_ids is None else [self.cols[i] for i in col_ids]
         return collect(cols, self.T, idx, start, L)
 
     def update(self, idx, newp):
+        if self.im is not None:
+            return self.im.update(self.priority, idx, newp)
         return update(self.priority, idx, newp)

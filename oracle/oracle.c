@@ -59,6 +59,25 @@
 #define ORC_PRIORITIZED 3
 #define ORC_TOPK        4
 
+/* Index manager state (see oracle_im_init). */
+#define ORC_IM_FREE      0
+#define ORC_IM_PENDING   1   /* allocated, being written */
+#define ORC_IM_COMMITTED 2
+
+typedef struct {
+    int64_t N;             /* indices (blocks per column table) */
+    int removal;           /* ORC_FIFO or ORC_LIFO */
+    int64_t max_sel;       /* preset maximum of selectable indices */
+    int64_t *free_q;       /* free indices, front first */
+    int64_t n_free;
+    int64_t *committed;    /* committed indices, oldest commit first */
+    int64_t n_committed;
+    int64_t n_pending;     /* allocated, not yet committed */
+    uint8_t *state;        /* ORC_IM_* per index */
+} orc_im;
+
+void oracle_im_free(orc_im *m);
+
 /* ------------------------------------------------------------------------ */
 /* splitmix64 (Steele, Lea & Flood, "Fast splittable pseudorandom number     */
 /* generators", OOPSLA 2014).  The generator state advances by the golden    */
@@ -151,8 +170,13 @@ static int orc_topk_cmp(const void *a, const void *b)
 /*   start[b] first timestep of the L-step window, uniform on [0, T-L]      */
 /*   w[b]     importance-sampling weight (prioritized) or 1, if w != NULL   */
 /* ------------------------------------------------------------------------ */
+/* With an index manager (below), `order` lists the committed slots, oldest */
+/* commit first, and n = norder; FIFO, LIFO and uniform then pick from that  */
+/* list.  With order == NULL the ring state above applies.                   */
+/* ------------------------------------------------------------------------ */
 int oracle_select(int strategy, const uint32_t *priority, int64_t N,
-                  uint64_t next_seq, int32_t T, int32_t B, int32_t L,
+                  uint64_t next_seq, const int64_t *order, int64_t norder,
+                  int32_t T, int32_t B, int32_t L,
                   uint64_t seed, float beta,
                   int64_t *idx, int32_t *start, float *w,
                   uint64_t *C_scratch /* N entries, prioritized only */)
@@ -164,7 +188,10 @@ int oracle_select(int strategy, const uint32_t *priority, int64_t N,
         return ORC_INVAL;
     if (strategy < ORC_FIFO || strategy > ORC_TOPK)
         return ORC_INVAL;
-    n = (next_seq < (uint64_t)N) ? (int64_t)next_seq : N;
+    if (order != NULL)
+        n = norder;
+    else
+        n = (next_seq < (uint64_t)N) ? (int64_t)next_seq : N;
     if (n == 0)
         return ORC_EMPTY;
 
@@ -174,17 +201,24 @@ int oracle_select(int strategy, const uint32_t *priority, int64_t N,
         if ((int64_t)B > n)
             return ORC_INSUFFICIENT;
         for (b = 0; b < B; b++) {
-            uint64_t k;   /* insertion number of the b-th selected trajectory */
-            if (strategy == ORC_FIFO)
-                k = next_seq - (uint64_t)n + (uint64_t)b;
-            else
-                k = next_seq - 1u - (uint64_t)b;
-            idx[b] = (int64_t)(k % (uint64_t)N);
+            if (order != NULL) {
+                idx[b] = strategy == ORC_FIFO ? order[b] : order[n - 1 - b];
+            } else {
+                uint64_t k;   /* insertion number of the b-th selected trajectory */
+                if (strategy == ORC_FIFO)
+                    k = next_seq - (uint64_t)n + (uint64_t)b;
+                else
+                    k = next_seq - 1u - (uint64_t)b;
+                idx[b] = (int64_t)(k % (uint64_t)N);
+            }
         }
     } else if (strategy == ORC_UNIFORM) {
-        /* Uniform over the live slots [0, n). */
-        for (b = 0; b < B; b++)
-            idx[b] = (int64_t)oracle_bounded(oracle_draw(seed, 2u * (uint64_t)b), (uint64_t)n);
+        /* Uniform over the n live trajectories: the live slots [0, n) of the
+         * ring, or the committed list of an index manager. */
+        for (b = 0; b < B; b++) {
+            int64_t r = (int64_t)oracle_bounded(oracle_draw(seed, 2u * (uint64_t)b), (uint64_t)n);
+            idx[b] = order != NULL ? order[r] : r;
+        }
     } else if (strategy == ORC_TOPK) {
         /* The B highest-priority selectable slots (priority > 0), higher
          * priority first, lower slot first among equals.  Missing draws
@@ -324,6 +358,146 @@ uint64_t oracle_insert(int32_t ncols, uint8_t *const *col_base, const int64_t *e
         priority[slot] = prio[r];
     }
     return next_seq + (uint64_t)n;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Index manager (Sec. 3.2): a block allocator with one queue of free        */
+/* indices (allocation dequeues, release enqueues) and a status table whose  */
+/* priority is 0 for indices that are free or still being written.          */
+/*                                                                          */
+/* Insertion (Sec. 3.2, trajectory insertion and deletion): `allocate`      */
+/* hands out free indices; the client writes the blocks of those indices in */
+/* place; `commit` sets their priorities and makes them selectable.  When   */
+/* an index is requested and none is free, or the number of selectable      */
+/* indices has reached the preset maximum, a victim is released by the      */
+/* removal strategy: FIFO releases the oldest committed index, LIFO the     */
+/* newest.                                                                   */
+/*                                                                          */
+/* Reading: pending (allocated, uncommitted) indices count toward the        */
+/* maximum, so a victim is released while committed + pending >= max_sel;   */
+/* with max_sel = N this is exactly "no free index".  Pending indices are    */
+/* never released.                                                           */
+/*                                                                          */
+/* Plain arrays and linear work: the committed list is kept oldest first    */
+/* and shifted on removal; the free queue likewise.                          */
+/* ------------------------------------------------------------------------ */
+int oracle_im_init(orc_im *m, int64_t N, int removal, int64_t max_sel)
+{
+    int64_t i;
+    m->free_q = NULL;
+    m->committed = NULL;
+    m->state = NULL;
+    if (N <= 0 || (removal != ORC_FIFO && removal != ORC_LIFO) || max_sel < 1 || max_sel > N)
+        return ORC_INVAL;
+    m->N = N;
+    m->removal = removal;
+    m->max_sel = max_sel;
+    m->free_q = (int64_t *)malloc(sizeof(int64_t) * (size_t)N);
+    m->committed = (int64_t *)malloc(sizeof(int64_t) * (size_t)N);
+    m->state = (uint8_t *)malloc((size_t)N);
+    if (m->free_q == NULL || m->committed == NULL || m->state == NULL) {
+        oracle_im_free(m);
+        return ORC_INVAL;
+    }
+    for (i = 0; i < N; i++) {
+        m->free_q[i] = i;            /* every index starts free, in index order */
+        m->state[i] = ORC_IM_FREE;
+    }
+    m->n_free = N;
+    m->n_committed = 0;
+    m->n_pending = 0;
+    return ORC_OK;
+}
+
+void oracle_im_free(orc_im *m)
+{
+    free(m->free_q);
+    free(m->committed);
+    free(m->state);
+    m->free_q = NULL;
+    m->committed = NULL;
+    m->state = NULL;
+}
+
+/* Release one victim by the removal strategy: its priority becomes 0 and
+ * the index joins the back of the free queue. */
+static void orc_im_release_victim(orc_im *m, uint32_t *priority)
+{
+    int64_t v, k;
+    if (m->removal == ORC_FIFO) {
+        v = m->committed[0];
+        for (k = 1; k < m->n_committed; k++)
+            m->committed[k - 1] = m->committed[k];
+    } else {
+        v = m->committed[m->n_committed - 1];
+    }
+    m->n_committed--;
+    m->state[v] = ORC_IM_FREE;
+    priority[v] = 0;
+    m->free_q[m->n_free++] = v;
+}
+
+/* Allocate n indices into idx_out, releasing victims as needed.  Fails
+ * with ORC_INSUFFICIENT, changing nothing, when the pending indices alone
+ * would exceed the maximum. */
+int oracle_im_allocate(orc_im *m, int64_t n, int64_t *idx_out, uint32_t *priority)
+{
+    int64_t r, k;
+    if (n < 0)
+        return ORC_INVAL;
+    if (m->n_pending + n > m->max_sel)
+        return ORC_INSUFFICIENT;
+    for (r = 0; r < n; r++) {
+        while (m->n_free == 0 || m->n_committed + m->n_pending >= m->max_sel)
+            orc_im_release_victim(m, priority);
+        idx_out[r] = m->free_q[0];
+        for (k = 1; k < m->n_free; k++)
+            m->free_q[k - 1] = m->free_q[k];
+        m->n_free--;
+        m->state[idx_out[r]] = ORC_IM_PENDING;
+        m->n_pending++;
+    }
+    return ORC_OK;
+}
+
+/* Commit n pending indices, in the given order, with their priorities.
+ * Every index must be pending and appear once; otherwise nothing changes. */
+int oracle_im_commit(orc_im *m, int64_t n, const int64_t *idx, const uint32_t *prio, uint32_t *priority)
+{
+    int64_t r, q;
+    if (n < 0)
+        return ORC_INVAL;
+    for (r = 0; r < n; r++) {
+        if (idx[r] < 0 || idx[r] >= m->N || m->state[idx[r]] != ORC_IM_PENDING)
+            return ORC_INVAL;
+        for (q = 0; q < r; q++)
+            if (idx[q] == idx[r])
+                return ORC_INVAL;
+    }
+    for (r = 0; r < n; r++) {
+        m->state[idx[r]] = ORC_IM_COMMITTED;
+        m->committed[m->n_committed++] = idx[r];
+        m->n_pending--;
+        priority[idx[r]] = prio[r];
+    }
+    return ORC_OK;
+}
+
+/* Priority update under an index manager: as oracle_update, except that an
+ * index that is not committed (released, or being written) keeps its zero
+ * priority, so a late update never makes it selectable. */
+int oracle_im_update(const orc_im *m, uint32_t *priority, const int64_t *idx, const uint32_t *newp, int32_t B)
+{
+    int32_t b;
+    if (B < 0)
+        return ORC_INVAL;
+    for (b = 0; b < B; b++)
+        if (idx[b] < 0 || idx[b] >= m->N)
+            return ORC_INVAL;
+    for (b = 0; b < B; b++)
+        if (m->state[idx[b]] == ORC_IM_COMMITTED)
+            priority[idx[b]] = newp[b];
+    return ORC_OK;
 }
 
 /* ------------------------------------------------------------------------ */
