@@ -89,7 +89,8 @@ typedef struct gear_table gear_table;
  * Column c is laid out as [capacity][T][elem_bytes[c]] bytes.  The store
  * also owns the uint32 priority array [capacity] (zero = not selectable,
  * Sec. 3.2 index manager) in HBM, and the scan, search and scatter scratch,
- * all sized by `capacity` at creation; no later call allocates.
+ * all sized by `capacity` at creation; no later call allocates except
+ * gear_table_use_allocator.
  * Errors: GEAR_E_INVAL, GEAR_E_NOMEM, GEAR_E_HIP.
  */
 int gear_table_create(const int64_t *elem_bytes, int32_t ncols, int64_t capacity, int32_t T,
@@ -119,6 +120,74 @@ int gear_table_destroy(gear_table *t);
  */
 int gear_insert(gear_table *t, int64_t n, const void *const *col_src, const uint32_t *priorities,
                 void *stream);
+/* On a table with an index manager, gear_insert is one gear_allocate of n,
+ * the row copies into the allocated blocks, and one gear_commit of the n
+ * indices with `priorities` (GEAR_E_INSUFFICIENT if pending + n would exceed
+ * the maximum). */
+
+/*
+ * Index manager (Sec. 3.2): a block allocator with one queue of free indices,
+ * and a status table in which the priority of an index that is free or still
+ * being written is zero.  A table with an index manager inserts by
+ * gear_allocate -> in-place writes -> gear_commit (Sec. 3.2, trajectory
+ * insertion and deletion) instead of the ring above; FIFO, LIFO and uniform
+ * selection then follow the commit order, and the live count is the number
+ * of committed indices.
+ */
+
+/*
+ * gear_table_use_allocator - give the table an index manager.  Must be
+ * called before anything is inserted.
+ *
+ *   removal         GEAR_FIFO (release the oldest commit) or GEAR_LIFO (the
+ *                   newest) when an index is requested and none is free, or
+ *                   when committed + pending indices have reached the maximum
+ *   max_selectable  the preset maximum, in [1, capacity]
+ *
+ * Allocates the manager's arrays: 4 + 1 bytes per slot in HBM and 9 bytes per
+ * slot of host memory, plus fixed staging buffers.  Every index starts free,
+ * in index order.  Errors: GEAR_E_INVAL, GEAR_E_NOMEM, GEAR_E_HIP.
+ */
+int gear_table_use_allocator(gear_table *t, int32_t removal, int64_t max_selectable);
+
+/*
+ * gear_allocate - request n indices for new trajectories (Sec. 3.2: the
+ * client asks the block allocator for free indices).  Indices come from the
+ * front of the free queue; whenever none is free, or committed + pending
+ * indices have reached the maximum, a victim is released first (its index
+ * joins the back of the free queue).
+ *
+ *   n        >= 0; pending + n must not exceed max_selectable
+ *   idx_out  host int64[n] receives the indices, in dequeue order
+ *
+ * The victims' priorities are zeroed by work enqueued on `stream`, before
+ * anything the caller enqueues later.  The blocks of index i in column c are
+ * base_c + i*T*elem_bytes[c] (gear_table_column); the caller fills them in
+ * place, ordered after this call's stream work, then commits.
+ * Errors: GEAR_E_INVAL (no index manager, n < 0, NULL idx_out),
+ * GEAR_E_INSUFFICIENT (pending would exceed the maximum; nothing changes),
+ * GEAR_E_HIP.
+ */
+int gear_allocate(gear_table *t, int64_t n, int64_t *idx_out, void *stream);
+
+/*
+ * gear_commit - make pending indices selectable (Sec. 3.2: commit updates
+ * the status table).  Sets their priorities and appends them to the commit
+ * order in the order given.
+ *
+ *   idx         host int64[n]; each must be pending (allocated, not yet
+ *               committed) and appear once
+ *   priorities  n uint32 values, host or device memory, valid until the
+ *               enqueued copies complete; 0 commits an unselectable index
+ *
+ * Errors: GEAR_E_INVAL (no index manager, an index not pending or repeated;
+ * nothing changes), GEAR_E_HIP.
+ */
+int gear_commit(gear_table *t, int64_t n, const int64_t *idx, const uint32_t *priorities, void *stream);
+
+/* gear_allocator_info - committed, pending and free index counts of a table
+ * with an index manager.  Any output may be NULL.  Errors: GEAR_E_INVAL. */
+int gear_allocator_info(const gear_table *t, int64_t *committed, int64_t *pending, int64_t *free_count);
 
 /*
  * gear_select - choose B trajectories and an L-step window in each (Sec. 1
@@ -184,11 +253,14 @@ int gear_collect(gear_table *t, const int64_t *d_idx, const int32_t *d_start, in
  * committed).  Applied as if in batch order: when a slot appears more than
  * once, the last occurrence's value wins.
  *
- *   d_idx            device int64[B], slots in [0, live count)
+ *   d_idx            device int64[B], slots in [0, live count) (a table
+ *                    with an index manager: [0, capacity))
  *   d_new_priorities device uint32[B]
  *   B                0 .. GEAR_MAX_BATCH
  *
- * An index outside [0, live count) is skipped and sets GEAR_STATUS_BAD_INDEX.
+ * An index outside that range is skipped and sets GEAR_STATUS_BAD_INDEX.  With
+ * an index manager, the update of an index that is not committed (released,
+ * or being written again) is dropped, so it never becomes selectable.
  * Errors: GEAR_E_INVAL, GEAR_E_HIP.
  */
 int gear_update_priorities(gear_table *t, const int64_t *d_idx, const uint32_t *d_new_priorities,
@@ -202,8 +274,9 @@ int gear_update_priorities(gear_table *t, const int64_t *d_idx, const uint32_t *
  */
 int gear_table_sync(gear_table *t, void *stream, int32_t *device_status);
 
-/* gear_table_info - host-side ring state: live count min(next_seq, capacity)
- * and the number of insertions so far.  Either output may be NULL. */
+/* gear_table_info - live count (min(next_seq, capacity) for a ring table,
+ * the committed count with an index manager) and the number of insertions
+ * (commits) so far.  Either output may be NULL. */
 int gear_table_info(const gear_table *t, int64_t *count, uint64_t *next_seq);
 
 /*

@@ -1,0 +1,274 @@
+// Index manager of a table (GEAR Sec. 3.2): a block allocator with one queue
+// of free indices and a status table whose priority is zero for indices that
+// are free or still being written.
+//
+// Insertion (Sec. 3.2, trajectory insertion and deletion):
+//   gear_allocate  dequeues free indices.  When none is free, or the
+//                  committed and pending indices have reached the preset
+//                  maximum, it first releases a victim by the removal
+//                  strategy (FIFO: the oldest commit, LIFO: the newest): the
+//                  victim's priority is zeroed on the device and its index
+//                  joins the back of the free queue.
+//   (the client writes the blocks of its indices in place, through the
+//    column base addresses)
+//   gear_commit    writes the priorities, marks the indices committed and
+//                  appends them to the commit-order ring on the device, so
+//                  they become selectable.
+//
+// The queue, the per-slot state and the commit order are host data: each
+// call's decisions are a few integer operations per index.  The device keeps
+// a copy of the commit-order ring (FIFO, LIFO and uniform selection read it)
+// and a committed flag per slot (priority updates of other slots are
+// dropped).  Index lists reach the device through a pinned staging buffer
+// that is reused only after the copy out of it has completed.
+#include <algorithm>
+#include <cstring>
+#include <new>
+
+#include "gear_internal.h"
+
+namespace gear {
+namespace {
+
+__global__ void evict_kernel(const int64_t* __restrict__ victims, int64_t n, uint32_t* __restrict__ prio,
+                             uint8_t* __restrict__ committed) {
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= n) return;
+    const int64_t i = victims[j];
+    prio[i] = 0u;
+    committed[i] = 0;
+}
+
+// Commit j of this chunk takes commit-order position pos0 + j (mod N).
+__global__ void commit_kernel(const int64_t* __restrict__ idx, const uint32_t* __restrict__ p, int64_t n,
+                              int64_t pos0, int64_t N, int32_t* __restrict__ order, uint32_t* __restrict__ prio,
+                              uint8_t* __restrict__ committed) {
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= n) return;
+    const int64_t i = idx[j];
+    prio[i] = p[j];
+    committed[i] = 1;
+    int64_t pos = pos0 + j;
+    if (pos >= N) pos -= N;
+    order[pos] = (int32_t)i;
+}
+
+// Copies `count` (<= kStageRows) host indices to t.stage_idx on stream s.
+hipError_t stage_indices(Table& t, const int64_t* host, int64_t count, hipStream_t s) {
+    hipError_t e = hipEventSynchronize(t.pin_free);  // the previous copy out of pin_idx is done
+    if (e != hipSuccess) return e;
+    std::memcpy(t.pin_idx, host, sizeof(int64_t) * (size_t)count);
+    e = hipMemcpyAsync(t.stage_idx, t.pin_idx, sizeof(int64_t) * (size_t)count, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return e;
+    return hipEventRecord(t.pin_free, s);
+}
+
+unsigned blocks_for(int64_t n) { return (unsigned)((n + 255) / 256); }
+
+// Releases one victim by the removal strategy (host state only).
+int64_t release_victim(Table& t) {
+    int64_t pos;
+    if (t.removal == GEAR_FIFO) {
+        pos = t.ord_head;
+        t.ord_head = t.ord_head + 1 == t.N ? 0 : t.ord_head + 1;
+    } else {
+        pos = (t.ord_head + t.n_committed - 1) % t.N;
+    }
+    const int32_t v = t.order_h[pos];
+    t.n_committed--;
+    t.slot_state[v] = kSlotFree;
+    t.free_q[(t.fq_head + t.n_free) % t.N] = v;
+    t.n_free++;
+    return v;
+}
+
+}  // namespace
+
+void free_index_manager(Table& t) {
+    (void)hipFree(t.order);
+    (void)hipFree(t.committed);
+    (void)hipFree(t.stage_idx);
+    (void)hipFree(t.stage_prio);
+    if (t.pin_idx) (void)hipHostFree(t.pin_idx);
+    if (t.pin_free) (void)hipEventDestroy(t.pin_free);
+    t.order = nullptr;
+    t.committed = nullptr;
+    t.stage_idx = nullptr;
+    t.stage_prio = nullptr;
+    t.pin_idx = nullptr;
+    t.pin_free = nullptr;
+    std::vector<int32_t>().swap(t.free_q);
+    std::vector<int32_t>().swap(t.order_h);
+    std::vector<uint8_t>().swap(t.slot_state);
+    t.managed = false;
+}
+
+int managed_insert(Table& t, int64_t n, const void* const* col_src, const uint32_t* priorities, hipStream_t s) {
+    if (t.n_pending + n > t.max_selectable)
+        return fail(GEAR_E_INSUFFICIENT, "gear_insert: more rows than the index manager can hold pending");
+    std::vector<int64_t> idx;
+    try {
+        idx.resize((size_t)n);
+    } catch (const std::bad_alloc&) {
+        return fail(GEAR_E_NOMEM, "gear_insert: host index list");
+    }
+    gear_table* h = reinterpret_cast<gear_table*>(&t);
+    int rc = gear_allocate(h, n, idx.data(), s);
+    if (rc != GEAR_OK) return rc;
+    // Write each row into its slot in place, one copy per run of consecutive slots.
+    for (int c = 0; c < t.ncols; c++) {
+        const size_t rb = (size_t)t.T * (size_t)t.elem_bytes[c];
+        uint8_t* base = t.residency == GEAR_HOST_PINNED ? t.col_host[c] : t.col_dev[c];
+        const uint8_t* src = static_cast<const uint8_t*>(col_src[c]);
+        int64_t r0 = 0;
+        while (r0 < n) {
+            int64_t r1 = r0 + 1;
+            while (r1 < n && idx[r1] == idx[r1 - 1] + 1) r1++;
+            hipError_t e = hipMemcpyAsync(base + (size_t)idx[r0] * rb, src + (size_t)r0 * rb,
+                                          (size_t)(r1 - r0) * rb, hipMemcpyDefault, s);
+            if (e != hipSuccess) return hip_fail(e, "gear_insert: row copy");
+            r0 = r1;
+        }
+    }
+    return gear_commit(h, n, idx.data(), priorities, s);
+}
+
+}  // namespace gear
+
+using gear::fail;
+using gear::hip_fail;
+using gear::Table;
+
+extern "C" int gear_table_use_allocator(gear_table* h, int32_t removal, int64_t max_selectable) {
+    if (h == nullptr) return fail(GEAR_E_INVAL, "gear_table_use_allocator: table is NULL");
+    Table* t = reinterpret_cast<Table*>(h);
+    if (removal != GEAR_FIFO && removal != GEAR_LIFO)
+        return fail(GEAR_E_INVAL, "gear_table_use_allocator: removal must be GEAR_FIFO or GEAR_LIFO");
+    if (max_selectable < 1 || max_selectable > t->N)
+        return fail(GEAR_E_INVAL, "gear_table_use_allocator: max_selectable must lie in [1, capacity]");
+    if (t->managed) return fail(GEAR_E_INVAL, "gear_table_use_allocator: the table already has an index manager");
+    if (t->next_seq != 0) return fail(GEAR_E_INVAL, "gear_table_use_allocator: the table already holds insertions");
+    gear::DeviceGuard guard(t->device);
+    if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_table_use_allocator: hipSetDevice");
+    try {
+        t->free_q.resize((size_t)t->N);
+        t->order_h.resize((size_t)t->N);
+        t->slot_state.assign((size_t)t->N, gear::kSlotFree);
+    } catch (const std::bad_alloc&) {
+        gear::free_index_manager(*t);
+        return fail(GEAR_E_NOMEM, "gear_table_use_allocator: host index arrays");
+    }
+    for (int64_t i = 0; i < t->N; i++) t->free_q[(size_t)i] = (int32_t)i;  // every index free, in index order
+    hipError_t e;
+    if ((e = hipMalloc(reinterpret_cast<void**>(&t->order), sizeof(int32_t) * (size_t)t->N)) != hipSuccess ||
+        (e = hipMalloc(reinterpret_cast<void**>(&t->committed), (size_t)t->N)) != hipSuccess ||
+        (e = hipMalloc(reinterpret_cast<void**>(&t->stage_idx), sizeof(int64_t) * gear::kStageRows)) != hipSuccess ||
+        (e = hipMalloc(reinterpret_cast<void**>(&t->stage_prio), sizeof(uint32_t) * gear::kStageRows)) != hipSuccess ||
+        (e = hipHostMalloc(reinterpret_cast<void**>(&t->pin_idx), sizeof(int64_t) * gear::kStageRows,
+                           hipHostMallocDefault)) != hipSuccess) {
+        gear::free_index_manager(*t);
+        return fail(GEAR_E_NOMEM, "gear_table_use_allocator: device arrays");
+    }
+    if ((e = hipEventCreateWithFlags(&t->pin_free, hipEventDisableTiming)) != hipSuccess ||
+        (e = hipMemset(t->committed, 0, (size_t)t->N)) != hipSuccess ||
+        (e = hipDeviceSynchronize()) != hipSuccess) {
+        gear::free_index_manager(*t);
+        return hip_fail(e, "gear_table_use_allocator: initialising");
+    }
+    t->fq_head = 0;
+    t->n_free = t->N;
+    t->ord_head = 0;
+    t->n_committed = 0;
+    t->n_pending = 0;
+    t->removal = removal;
+    t->max_selectable = max_selectable;
+    t->managed = true;
+    return GEAR_OK;
+}
+
+extern "C" int gear_allocate(gear_table* h, int64_t n, int64_t* idx_out, void* stream) {
+    if (h == nullptr) return fail(GEAR_E_INVAL, "gear_allocate: table is NULL");
+    Table* t = reinterpret_cast<Table*>(h);
+    if (!t->managed) return fail(GEAR_E_INVAL, "gear_allocate: the table has no index manager");
+    if (n < 0) return fail(GEAR_E_INVAL, "gear_allocate: n < 0");
+    if (n == 0) return GEAR_OK;
+    if (idx_out == nullptr) return fail(GEAR_E_INVAL, "gear_allocate: idx_out is NULL");
+    if (t->n_pending + n > t->max_selectable)
+        return fail(GEAR_E_INSUFFICIENT, "gear_allocate: pending indices would exceed the maximum");
+    gear::DeviceGuard guard(t->device);
+    if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_allocate: hipSetDevice");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    std::vector<int64_t> victims;
+    for (int64_t r = 0; r < n; r++) {
+        // Pending stays below the maximum here, so a victim exists whenever one is needed.
+        while (t->n_free == 0 || t->n_committed + t->n_pending >= t->max_selectable)
+            victims.push_back(gear::release_victim(*t));
+        const int32_t i = t->free_q[(size_t)t->fq_head];
+        t->fq_head = t->fq_head + 1 == t->N ? 0 : t->fq_head + 1;
+        t->n_free--;
+        t->slot_state[(size_t)i] = gear::kSlotPending;
+        t->n_pending++;
+        idx_out[r] = i;
+    }
+    // Victims become unselectable before the caller writes into any slot.
+    for (size_t off = 0; off < victims.size(); off += (size_t)gear::kStageRows) {
+        const int64_t cnt = (int64_t)std::min(victims.size() - off, (size_t)gear::kStageRows);
+        hipError_t e = gear::stage_indices(*t, victims.data() + off, cnt, s);
+        if (e != hipSuccess) return hip_fail(e, "gear_allocate: staging victims");
+        hipLaunchKernelGGL(gear::evict_kernel, dim3(gear::blocks_for(cnt)), dim3(256), 0, s, t->stage_idx, cnt,
+                           t->priority, t->committed);
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "gear_allocate: launch");
+    }
+    if (!victims.empty()) t->cdf_dirty = true;
+    return GEAR_OK;
+}
+
+extern "C" int gear_commit(gear_table* h, int64_t n, const int64_t* idx, const uint32_t* priorities, void* stream) {
+    if (h == nullptr) return fail(GEAR_E_INVAL, "gear_commit: table is NULL");
+    Table* t = reinterpret_cast<Table*>(h);
+    if (!t->managed) return fail(GEAR_E_INVAL, "gear_commit: the table has no index manager");
+    if (n < 0) return fail(GEAR_E_INVAL, "gear_commit: n < 0");
+    if (n == 0) return GEAR_OK;
+    if (idx == nullptr || priorities == nullptr) return fail(GEAR_E_INVAL, "gear_commit: NULL pointer argument");
+    // Every index pending and listed once; marks are undone on any failure.
+    int64_t r = 0;
+    for (; r < n; r++) {
+        if (idx[r] < 0 || idx[r] >= t->N || t->slot_state[(size_t)idx[r]] != gear::kSlotPending) break;
+        t->slot_state[(size_t)idx[r]] = gear::kSlotMark;
+    }
+    for (int64_t q = 0; q < r; q++) t->slot_state[(size_t)idx[q]] = gear::kSlotPending;
+    if (r < n) return fail(GEAR_E_INVAL, "gear_commit: an index is not pending or is listed twice");
+    gear::DeviceGuard guard(t->device);
+    if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_commit: hipSetDevice");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    for (int64_t off = 0; off < n; off += gear::kStageRows) {
+        const int64_t cnt = std::min(n - off, gear::kStageRows);
+        hipError_t e = gear::stage_indices(*t, idx + off, cnt, s);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(t->stage_prio, priorities + off, sizeof(uint32_t) * (size_t)cnt, hipMemcpyDefault, s);
+        if (e != hipSuccess) return hip_fail(e, "gear_commit: staging");
+        const int64_t pos0 = (t->ord_head + t->n_committed) % t->N;
+        hipLaunchKernelGGL(gear::commit_kernel, dim3(gear::blocks_for(cnt)), dim3(256), 0, s, t->stage_idx,
+                           t->stage_prio, cnt, pos0, t->N, t->order, t->priority, t->committed);
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "gear_commit: launch");
+        for (int64_t j = off; j < off + cnt; j++) {
+            t->slot_state[(size_t)idx[j]] = gear::kSlotCommitted;
+            t->order_h[(size_t)((t->ord_head + t->n_committed) % t->N)] = (int32_t)idx[j];
+            t->n_committed++;
+            t->n_pending--;
+        }
+    }
+    t->next_seq += (uint64_t)n;
+    t->cdf_dirty = true;
+    return GEAR_OK;
+}
+
+extern "C" int gear_allocator_info(const gear_table* h, int64_t* committed, int64_t* pending, int64_t* free_count) {
+    if (h == nullptr) return fail(GEAR_E_INVAL, "gear_allocator_info: table is NULL");
+    const Table* t = reinterpret_cast<const Table*>(h);
+    if (!t->managed) return fail(GEAR_E_INVAL, "gear_allocator_info: the table has no index manager");
+    if (committed) *committed = t->n_committed;
+    if (pending) *pending = t->n_pending;
+    if (free_count) *free_count = t->n_free;
+    return GEAR_OK;
+}

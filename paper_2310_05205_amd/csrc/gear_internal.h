@@ -23,13 +23,17 @@ constexpr int kMaxLevels = 6;
 // The search runs at most this many workgroups; each leaves the smallest
 // priority its draws selected in one slot of Table::wg_min.
 constexpr int kSearchMaxGrid = 2048;
-// TopK: at most this many workgroups per pass, and at most this many draws
-// (the final sort holds all K keys in one workgroup's LDS).
+// TopK: at most this many workgroups per digit pass.
 constexpr int kTopkMaxGrid = 256;
 constexpr int kTopkBins = 4096;       // bins of one TopK digit pass (12-bit digits)
 constexpr int kTopkStateWords = 8;
 constexpr int kTopkRankBlock = 512;    // keys one TopK rank workgroup compares against
 constexpr int kTopkMaxK = GEAR_MAX_TOPK;
+// Index manager: index lists move to the device in chunks of this many.
+constexpr int64_t kStageRows = 1 << 16;
+
+// Per-slot state of the index manager (host side).
+enum : uint8_t { kSlotFree = 0, kSlotPending = 1, kSlotCommitted = 2, kSlotMark = 3 };
 
 struct Table {
     int device = 0;
@@ -63,6 +67,25 @@ struct Table {
     uint32_t* topk_hist = nullptr;    // [3][kTopkBins] digit histograms, zero between calls
     uint32_t* topk_state = nullptr;   // [kTopkStateWords] selection state after the digit passes
     uint32_t* topk_local = nullptr;   // [3][kTopkMaxGrid][kTopkBins] per-workgroup suffix sums of each digit pass
+    // Index manager (allocate / commit insertion), off for ring tables.  The
+    // host keeps the free-index queue, every slot's state and the committed
+    // slots in commit order (a ring: ord_head is the oldest); the device
+    // keeps the same commit-order ring and a committed flag per slot.
+    bool managed = false;
+    int32_t removal = GEAR_FIFO;
+    int64_t max_selectable = 0;
+    std::vector<int32_t> free_q;      // ring [N], front at fq_head
+    int64_t fq_head = 0, n_free = 0;
+    std::vector<uint8_t> slot_state;  // kSlot* per slot
+    std::vector<int32_t> order_h;     // ring [N] of committed slots, oldest at ord_head
+    int64_t ord_head = 0, n_committed = 0, n_pending = 0;
+    int32_t* order = nullptr;         // device copy of order_h (same positions)
+    uint8_t* committed = nullptr;     // device [N]: 1 for committed slots
+    int64_t* stage_idx = nullptr;     // device staging [kStageRows]
+    uint32_t* stage_prio = nullptr;   // device staging [kStageRows]
+    int64_t* pin_idx = nullptr;       // pinned host staging [kStageRows]
+    hipEvent_t pin_free = nullptr;    // recorded after the last copy out of pin_idx
+
     uint64_t* topk_keys = nullptr;    // [kTopkMaxK] selected keys (p << 32 | ~slot), equal priorities in slot order
     uint32_t* topk_rank = nullptr;    // [kTopkMaxK] place of each key in descending order
 };
@@ -96,5 +119,15 @@ hipError_t launch_simple_select(Table& t, int32_t strategy, int32_t B, int32_t L
 // slot into the sum tree the last scan filled.
 hipError_t launch_scatter(Table& t, const int64_t* idx, const uint32_t* newp, int32_t B, bool maintain_tree,
                           hipStream_t s);
+// Index manager: release the memory of a managed table's extra arrays.
+void free_index_manager(Table& t);
+// Managed insertion used by gear_insert: allocate n, copy the rows into the
+// allocated slots, commit them with their priorities.
+int managed_insert(Table& t, int64_t n, const void* const* col_src, const uint32_t* priorities, hipStream_t s);
+// Live count of a table: committed slots (managed) or min(next_seq, N) (ring).
+inline int64_t live_count(const Table& t) {
+    if (t.managed) return t.n_committed;
+    return t.next_seq < (uint64_t)t.N ? (int64_t)t.next_seq : t.N;
+}
 
 }  // namespace gear

@@ -221,23 +221,32 @@ __global__ __launch_bounds__(256) void is_weights_kernel(int32_t B, double beta,
     w[b] = (pb == 0u || m == 0u) ? 0.0f : (float)pow((double)m / (double)pb, beta);
 }
 
-// FIFO / LIFO: ring arithmetic from the oldest / newest live slot.
-// Uniform: floor(u * n / 2^64) over the n live slots.
-__global__ void simple_select_kernel(int strategy, int32_t B, int64_t N, int64_t live, int64_t oldest_slot,
-                                     int64_t newest_slot, uint64_t span, uint64_t seed, int64_t* __restrict__ idx,
-                                     int32_t* __restrict__ start, float* __restrict__ w) {
+// FIFO / LIFO: ring arithmetic from the oldest / newest live position.
+// Uniform: r = floor(u * n / 2^64) over the n live trajectories.
+// A ring table's positions are its slots, and its live slots are [0, n).
+// A managed table (index manager) reads the slot at each position of its
+// commit-order ring `order`, oldest commit at `oldest`.
+__global__ void simple_select_kernel(int strategy, int32_t B, int64_t N, int64_t live, int64_t oldest,
+                                     int64_t newest, const int32_t* __restrict__ order, uint64_t span,
+                                     uint64_t seed, int64_t* __restrict__ idx, int32_t* __restrict__ start,
+                                     float* __restrict__ w) {
     const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= B) return;
     int64_t i;
     if (strategy == GEAR_FIFO) {
-        i = oldest_slot + b;
+        i = oldest + b;
         if (i >= N) i -= N;
     } else if (strategy == GEAR_LIFO) {
-        i = newest_slot - b;
+        i = newest - b;
         if (i < 0) i += N;
     } else {
         i = (int64_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b), (uint64_t)live);
+        if (order) {
+            i += oldest;
+            if (i >= N) i -= N;
+        }
     }
+    if (order) i = order[i];
     idx[b] = i;
     start[b] = (int32_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b + 1), span);
     if (w) w[b] = 1.0f;
@@ -296,11 +305,18 @@ hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, f
 
 hipError_t launch_simple_select(Table& t, int32_t strategy, int32_t B, int32_t L, uint64_t seed, int64_t* idx,
                                 int32_t* start, float* w, hipStream_t s) {
-    const int64_t live = t.next_seq < (uint64_t)t.N ? (int64_t)t.next_seq : t.N;
-    const int64_t oldest = (int64_t)((t.next_seq - (uint64_t)live) % (uint64_t)t.N);
-    const int64_t newest = (int64_t)((t.next_seq - 1) % (uint64_t)t.N);
+    const int64_t live = live_count(t);
+    int64_t oldest, newest;
+    if (t.managed) {
+        oldest = t.ord_head;
+        newest = (t.ord_head + live - 1) % t.N;
+    } else {
+        oldest = (int64_t)((t.next_seq - (uint64_t)live) % (uint64_t)t.N);
+        newest = (int64_t)((t.next_seq - 1) % (uint64_t)t.N);
+    }
     hipLaunchKernelGGL(simple_select_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s, strategy, B, t.N,
-                       live, oldest, newest, (uint64_t)(t.T - L + 1), seed, idx, start, w);
+                       live, oldest, newest, t.managed ? t.order : nullptr, (uint64_t)(t.T - L + 1), seed, idx,
+                       start, w);
     return hipGetLastError();
 }
 
@@ -319,7 +335,7 @@ extern "C" int gear_select(gear_table* h, int32_t strategy, int32_t B, int32_t L
     if (L < 1 || L > t->T) return fail(GEAR_E_INVAL, "gear_select: L must lie in [1, T]");
     if (d_idx == nullptr || d_start == nullptr) return fail(GEAR_E_INVAL, "gear_select: output pointer is NULL");
     if (!(beta == beta)) return fail(GEAR_E_INVAL, "gear_select: beta is NaN");
-    const int64_t live = t->next_seq < (uint64_t)t->N ? (int64_t)t->next_seq : t->N;
+    const int64_t live = gear::live_count(*t);
     if (live == 0) return fail(GEAR_E_EMPTY, "gear_select: nothing inserted");
     if ((strategy == GEAR_FIFO || strategy == GEAR_LIFO) && (int64_t)B > live)
         return fail(GEAR_E_INSUFFICIENT, "gear_select: FIFO/LIFO batch larger than the live count");

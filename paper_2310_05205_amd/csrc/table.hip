@@ -48,6 +48,7 @@ namespace {
 
 void free_table(Table* t) {
     if (!t) return;
+    gear::free_index_manager(*t);
     for (int c = 0; c < t->ncols; c++) {
         if (t->residency == GEAR_HOST_PINNED) {
             if (t->col_host[c]) (void)hipHostFree(t->col_host[c]);
@@ -221,6 +222,7 @@ extern "C" int gear_insert(gear_table* h, int64_t n, const void* const* col_src,
     gear::DeviceGuard guard(t->device);
     if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_insert: hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (t->managed) return gear::managed_insert(*t, n, col_src, priorities, s);
 
     // Rows written one after another into slot k mod N: only the last N
     // of a longer batch survive, so copy those.
@@ -274,7 +276,7 @@ extern "C" int gear_table_sync(gear_table* h, void* stream, int32_t* device_stat
 extern "C" int gear_table_info(const gear_table* h, int64_t* count, uint64_t* next_seq) {
     if (h == nullptr) return fail(GEAR_E_INVAL, "gear_table_info: table is NULL");
     const Table* t = reinterpret_cast<const Table*>(h);
-    if (count) *count = t->next_seq < (uint64_t)t->N ? (int64_t)t->next_seq : t->N;
+    if (count) *count = gear::live_count(*t);
     if (next_seq) *next_seq = t->next_seq;
     return GEAR_OK;
 }

@@ -58,9 +58,13 @@ __device__ inline void add_u64(uint64_t* p, uint64_t d) {
     atomicAdd(reinterpret_cast<unsigned long long*>(p), (unsigned long long)d);
 }
 
+// `live`: indices at or past it are invalid.  `committed` (managed tables
+// only, else NULL): an index whose flag is 0 is released or still being
+// written; its update is dropped, so it never becomes selectable.
 __global__ __launch_bounds__(kHashThreads) void scatter_lds_kernel(const int64_t* __restrict__ idx,
                                                                    const uint32_t* __restrict__ newp, int32_t B,
-                                                                   int64_t live, uint32_t* __restrict__ prio,
+                                                                   int64_t live, const uint8_t* __restrict__ committed,
+                                                                   uint32_t* __restrict__ prio,
                                                                    uint32_t* status, Tree tree) {
     __shared__ uint32_t key[kHashSize];
     __shared__ uint32_t tag[kHashSize];
@@ -89,7 +93,8 @@ __global__ __launch_bounds__(kHashThreads) void scatter_lds_kernel(const int64_t
         const int b = threadIdx.x + k * kHashThreads;
         const bool valid = b < B && slot[k] >= 0 && slot[k] < live;
         if (b < B && !valid && blockIdx.x == 0) bad = true;
-        mine[k] = valid && (((uint32_t)slot[k] * 0x85EBCA6Bu) >> (32 - kPartBits)) == blockIdx.x;
+        mine[k] = valid && (((uint32_t)slot[k] * 0x85EBCA6Bu) >> (32 - kPartBits)) == blockIdx.x &&
+                  (committed == nullptr || committed[slot[k]] != 0);
         old[k] = (tree.maintain && mine[k]) ? prio[slot[k]] : 0u;
     }
     __syncthreads();
@@ -138,8 +143,8 @@ __global__ __launch_bounds__(kHashThreads) void scatter_lds_kernel(const int64_t
     }
 }
 
-__global__ void scatter_tag_kernel(const int64_t* __restrict__ idx, int32_t B, int64_t live, uint32_t* tag,
-                                   uint32_t* status) {
+__global__ void scatter_tag_kernel(const int64_t* __restrict__ idx, int32_t B, int64_t live,
+                                   const uint8_t* __restrict__ committed, uint32_t* tag, uint32_t* status) {
     const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= B) return;
     const int64_t i = idx[b];
@@ -147,6 +152,7 @@ __global__ void scatter_tag_kernel(const int64_t* __restrict__ idx, int32_t B, i
         atomicOr(status, GEAR_STATUS_BAD_INDEX);
         return;
     }
+    if (committed != nullptr && committed[i] == 0) return;
     atomicMax(tag + i, (uint32_t)(b + 1));
 }
 
@@ -156,6 +162,7 @@ __global__ void scatter_apply_kernel(const int64_t* __restrict__ idx, const uint
     if (b >= B) return;
     const int64_t i = idx[b];
     if (i < 0 || i >= live) return;
+    // Dropped updates of uncommitted slots never raised the tag, so it is 0.
     if (tag[i] == (uint32_t)(b + 1)) {
         const uint32_t old = prio[i];
         prio[i] = newp[b];
@@ -186,15 +193,18 @@ Tree tree_of(const Table& t, bool maintain) {
 
 hipError_t launch_scatter(Table& t, const int64_t* idx, const uint32_t* newp, int32_t B, bool maintain_tree,
                           hipStream_t s) {
-    const int64_t live = t.next_seq < (uint64_t)t.N ? (int64_t)t.next_seq : t.N;
+    // Ring tables: slots [0, live count); managed tables: any slot, updates
+    // of uncommitted ones dropped.
+    const int64_t live = t.managed ? t.N : live_count(t);
+    const uint8_t* committed = t.managed ? t.committed : nullptr;
     const Tree tree = tree_of(t, maintain_tree);
     if (B <= kHashMaxBatch) {
         hipLaunchKernelGGL(scatter_lds_kernel, dim3(kParts), dim3(kHashThreads), 0, s, idx, newp, B, live,
-                           t.priority, t.status, tree);
+                           committed, t.priority, t.status, tree);
         return hipGetLastError();
     }
     const unsigned grid = (unsigned)((B + 255) / 256);
-    hipLaunchKernelGGL(scatter_tag_kernel, dim3(grid), dim3(256), 0, s, idx, B, live, t.tag, t.status);
+    hipLaunchKernelGGL(scatter_tag_kernel, dim3(grid), dim3(256), 0, s, idx, B, live, committed, t.tag, t.status);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(scatter_apply_kernel, dim3(grid), dim3(256), 0, s, idx, newp, B, live, t.tag, t.priority,

@@ -63,9 +63,15 @@ def lib():
         L.gear_table_column.argtypes = [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(i64)]
         L.gear_table_priorities.argtypes = [vp, ctypes.POINTER(vp)]
         L.gear_table_set_options.argtypes = [vp, ctypes.c_uint32]
+        L.gear_table_use_allocator.argtypes = [vp, i32, i64]
+        L.gear_allocate.argtypes = [vp, i64, vp, vp]
+        L.gear_commit.argtypes = [vp, i64, vp, vp, vp]
+        pi64 = ctypes.POINTER(i64)
+        L.gear_allocator_info.argtypes = [vp, pi64, pi64, pi64]
         for name in ["gear_table_create", "gear_table_destroy", "gear_insert", "gear_select", "gear_collect",
                      "gear_update_priorities", "gear_table_sync", "gear_table_info", "gear_table_column",
-                     "gear_table_priorities", "gear_table_set_options"]:
+                     "gear_table_priorities", "gear_table_set_options", "gear_table_use_allocator",
+                     "gear_allocate", "gear_commit", "gear_allocator_info"]:
             getattr(L, name).restype = ctypes.c_int
         L.gear_last_error.argtypes = []
         L.gear_last_error.restype = ctypes.c_char_p
@@ -154,6 +160,39 @@ def gear_table_priorities(table):
     return p.value
 
 
+def gear_table_use_allocator(table, removal, max_selectable):
+    _check(lib().gear_table_use_allocator(table, int(removal), int(max_selectable)))
+
+
+def gear_allocate(table, n, stream=0):
+    """Returns the n allocated indices as a host int64 numpy array."""
+    import numpy as np
+    idx = np.zeros(max(int(n), 1), dtype=np.int64)
+    _check(lib().gear_allocate(table, int(n), idx.ctypes.data, stream))
+    return idx[:int(n)]
+
+
+def gear_commit(table, idx, priorities, stream=0):
+    """idx: host int64 numpy array; priorities: pointer (host or device)."""
+    import numpy as np
+    idx = np.ascontiguousarray(idx, dtype=np.int64)
+    _check(lib().gear_commit(table, idx.size, idx.ctypes.data, priorities, stream))
+
+
+def gear_allocator_info(table):
+    c, p, f = ctypes.c_int64(0), ctypes.c_int64(0), ctypes.c_int64(0)
+    _check(lib().gear_allocator_info(table, ctypes.byref(c), ctypes.byref(p), ctypes.byref(f)))
+    return c.value, p.value, f.value
+
+
+class _DeviceBytes:
+    """Describes device memory to torch.as_tensor (array-interface protocol)."""
+
+    def __init__(self, ptr, shape):
+        self.__cuda_array_interface__ = {"shape": tuple(shape), "typestr": "|u1", "data": (int(ptr), False),
+                                         "strides": None, "version": 2}
+
+
 class Table:
     """A replay store over torch tensors.
 
@@ -220,6 +259,35 @@ class Table:
 
     def set_options(self, options):
         gear_table_set_options(self.handle, options)
+
+    def use_allocator(self, removal, max_selectable=None):
+        """Switch to allocate/commit insertion with FIFO or LIFO removal."""
+        gear_table_use_allocator(self.handle, removal, self.capacity if max_selectable is None else max_selectable)
+
+    def allocate(self, n, stream=None):
+        """n free indices (host int64 array); victims are released on the stream."""
+        return gear_allocate(self.handle, n, self._stream(stream))
+
+    def commit(self, idx, priorities, stream=None):
+        """Commit pending indices (host int64) with uint32 priorities (host or device)."""
+        gear_commit(self.handle, idx, _data_ptr(priorities), self._stream(stream))
+
+    def allocator_info(self):
+        return gear_allocator_info(self.handle)
+
+    def column_view(self, c):
+        """Column c's blocks in place, [capacity, T*E_c] bytes: a torch uint8
+        tensor over the table's HBM (device tables) or a numpy array over its
+        pinned host memory.  Writing rows of allocated indices through it is
+        the in-place insertion path; the view must not outlive the table."""
+        import numpy as np
+        base, host, eb = gear_table_column(self.handle, c)
+        shape = (self.capacity, self.T * eb)
+        if self.residency == GEAR_HOST_PINNED:
+            buf = (ctypes.c_uint8 * (shape[0] * shape[1])).from_address(host)
+            return np.ctypeslib.as_array(buf).reshape(shape)
+        torch = self._torch
+        return torch.as_tensor(_DeviceBytes(base, shape), device=torch.device("cuda", self.device))
 
     def sync(self, stream=None):
         return gear_table_sync(self.handle, self._stream(stream))

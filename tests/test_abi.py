@@ -54,6 +54,10 @@ def test_argument_validation_without_device():
     assert lib.gear_table_sync(None, None, None) == gear.GEAR_E_INVAL
     assert lib.gear_table_info(None, None, None) == gear.GEAR_E_INVAL
     assert lib.gear_table_destroy(None) == gear.GEAR_OK
+    assert lib.gear_table_use_allocator(None, 0, 1) == gear.GEAR_E_INVAL
+    assert lib.gear_allocate(None, 1, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_commit(None, 1, None, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_allocator_info(None, None, None, None) == gear.GEAR_E_INVAL
     with pytest.raises(gear.GearError) as e:
         gear.gear_table_create([4], 16, 0)
     assert e.value.code == gear.GEAR_E_INVAL
