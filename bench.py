@@ -13,7 +13,8 @@ against its bandwidth peak from HIP events around each gather launch in the
 timed region; `cpu_baseline` is the plain CPU oracle timed on a bounded
 sample of the same workload.
 
-  python bench.py [--steps K] [--warmup W] [--workload mat|gato-host|dt|tiny|select-stress]
+  python bench.py [--steps K] [--warmup W] [--workload mat|gato-host|dt|tiny|select-stress|topk]
+  python bench.py --workload mat-insert   # insertion through the index manager (own metric)
   python bench.py --calibrate     # plain copy kernel of known size, for counter scaling
   python bench.py --ceilings      # HBM read / write / copy rates of plain kernels
 """
@@ -80,7 +81,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="mat", choices=["mat", "gato-host", "dt", "tiny", "select-stress", "topk"])
+    ap.add_argument("--workload", default="mat",
+                    choices=["mat", "gato-host", "dt", "tiny", "select-stress", "topk", "mat-insert"])
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
     ap.add_argument("--incremental", action="store_true",
                     help="keep the selection sum tree current across updates (no rescan per step)")
@@ -204,6 +206,122 @@ def cpu_baseline(w, target_s):
                       % (reps, {3: "prioritized", 4: "TopK"}.get(strat, "select"), w.N, w.B, w.L, el)}
 
 
+def run_insert(args):
+    """Insertion through the index manager on the MAT-shaped HBM table, full
+    and in steady state (every new trajectory releases the oldest, FIFO).
+    One step: allocate B indices (victims' priorities zeroed on the device),
+    write B new trajectories in place through the column views (the client's
+    scatter, here torch indexing from device-resident rows), commit B with
+    device-side priorities.  Prints one JSON line with its own metric."""
+    import numpy as np
+    import torch
+
+    import gen
+    from gen import configs
+    from gen.fill import fill_table
+    from paper_2310_05205_amd import gear
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    w = configs.MAT
+    dev = torch.device("cuda", 0)
+    sh = torch.cuda.current_stream(dev).cuda_stream
+    t = gear.Table(w.elem_bytes, w.N, w.T, gear.GEAR_DEVICE, 0)
+    t.use_allocator(gear.GEAR_FIFO, w.N)
+    fill_table(w, lambda n, ptrs, prio: t.insert(ptrs, prio), device=0)
+    B, K, W = w.B, args.steps, args.warmup
+    # B new trajectories, generated in HBM: insertions N .. N+B-1 of the workload.
+    rows = [torch.empty((B, w.T * c.elem_bytes), dtype=torch.uint8, device=dev) for c in w.columns]
+    for ci, c in enumerate(w.columns):
+        gen.fill_rows_gpu(c, ci, w.seed, w.T, w.n_insert, B, rows[ci].data_ptr(), sh)
+    prio = torch.from_numpy(gen.insert_priorities(w.prio, w.seed, w.n_insert, B)).to(dev)
+    views = [t.column_view(c) for c in range(len(w.columns))]
+    hev = HipEvents()
+
+    def step(ev=None):
+        h0 = time.perf_counter()
+        if ev:
+            hev.record(ev[0], sh)
+        idx = t.allocate(B)
+        if ev:
+            hev.record(ev[1], sh)
+        h1 = time.perf_counter()
+        d_idx = torch.from_numpy(idx).to(dev)
+        for c, r in enumerate(rows):
+            views[c][d_idx] = r
+        if ev:
+            hev.record(ev[2], sh)
+        h2 = time.perf_counter()
+        t.commit(idx, prio)
+        if ev:
+            hev.record(ev[3], sh)
+        h3 = time.perf_counter()
+        return h1 - h0, h3 - h2
+
+    for _ in range(W):
+        step()
+    torch.cuda.synchronize()
+    evs = [[hev.create() for _ in range(4)] for _ in range(K)]
+    host_alloc, host_commit = [], []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        a, c = step(evs[k])
+        host_alloc.append(a)
+        host_commit.append(c)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    if t.sync() != 0:
+        raise SystemExit("device status set during the insert steps")
+    committed, pending, free = t.allocator_info()
+    assert committed == w.N and pending == 0
+    alloc_ms = float(np.mean([hev.elapsed_ms(e[0], e[1]) for e in evs]))
+    write_ms = float(np.mean([hev.elapsed_ms(e[1], e[2]) for e in evs]))
+    commit_ms = float(np.mean([hev.elapsed_ms(e[2], e[3]) for e in evs]))
+
+    # The library's own insertion: gear_insert = allocate, row copies into the
+    # allocated blocks (one per run of consecutive slots), commit.
+    ptrs = [r.data_ptr() for r in rows]
+    for _ in range(W):
+        t.insert(ptrs, prio)
+    torch.cuda.synchronize()
+    iev = [(hev.create(), hev.create()) for _ in range(K)]
+    t1 = time.perf_counter()
+    for k in range(K):
+        hev.record(iev[k][0], sh)
+        t.insert(ptrs, prio)
+        hev.record(iev[k][1], sh)
+    torch.cuda.synchronize()
+    wall_insert = time.perf_counter() - t1
+    ins_ms = float(np.mean([hev.elapsed_ms(a, b) for a, b in iev]))
+    if t.sync() != 0:
+        raise SystemExit("device status set during the gear_insert steps")
+    hev.close()
+    row_bytes = w.T * sum(w.elem_bytes)
+    line = {
+        "metric": "trajectories inserted/sec through allocate + in-place write + commit",
+        "value": round(B * K / wall, 1), "unit": "trajectories/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(wall * 1e3 / K, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u8", "data": "synthetic",
+        "config": {"workload": "mat-insert N=500000 T=200 B=8192 (FIFO removal, table full)", "N": w.N,
+                   "T": w.T, "B": B, "elem_bytes": w.elem_bytes, "table_bytes": w.table_bytes,
+                   "parallelism": "1 GPU"},
+        "trajectory_steps_per_s": round(B * w.T * K / wall, 1),
+        "stages_ms": {"allocate": round(alloc_ms, 5), "write": round(write_ms, 5), "commit": round(commit_ms, 5),
+                      "note": "HIP events around each stage in the timed steps; write is the client's scatter"},
+        "host_ms": {"allocate": round(1e3 * float(np.mean(host_alloc)), 4),
+                    "commit": round(1e3 * float(np.mean(host_commit)), 4)},
+        "write_GBps": round(2 * B * row_bytes / (write_ms * 1e-3) / 1e9, 1),
+        "gear_insert": {"trajectories_per_s": round(B * K / wall_insert, 1), "ms_per_call": round(ins_ms, 5),
+                        "copy_GBps": round(2 * B * row_bytes / (ins_ms * 1e-3) / 1e9, 1),
+                        "note": "gear_insert of the same B device-resident rows: allocate, one copy per run of "
+                                "consecutive slots per column, commit"},
+        "roofline": None, "cpu_baseline": None,
+    }
+    t.close()
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -216,6 +334,9 @@ def main():
         return
     if args.ceilings:
         ceilings()
+        return
+    if args.workload == "mat-insert":
+        run_insert(args)
         return
 
     import numpy as np

@@ -19,8 +19,9 @@
 // call's decisions are a few integer operations per index.  The device keeps
 // a copy of the commit-order ring (FIFO, LIFO and uniform selection read it)
 // and a committed flag per slot (priority updates of other slots are
-// dropped).  Index lists reach the device through a pinned staging buffer
-// that is reused only after the copy out of it has completed.
+// dropped).  Index lists reach the device through a ring of pinned staging
+// buffers; a buffer is refilled only after the copy out of it has completed,
+// so the host waits only when every buffer still has a copy in flight.
 #include <algorithm>
 #include <cstring>
 #include <new>
@@ -54,13 +55,18 @@ __global__ void commit_kernel(const int64_t* __restrict__ idx, const uint32_t* _
 }
 
 // Copies `count` (<= kStageRows) host indices to t.stage_idx on stream s.
+// The device buffer is reused in stream order: this copy runs after the
+// kernels that read the previous chunk.
 hipError_t stage_indices(Table& t, const int64_t* host, int64_t count, hipStream_t s) {
-    hipError_t e = hipEventSynchronize(t.pin_free);  // the previous copy out of pin_idx is done
+    const int slot = t.pin_next;
+    t.pin_next = (slot + 1) % kStageSlots;
+    int64_t* pin = t.pin_idx + (size_t)slot * kStageRows;
+    hipError_t e = hipEventSynchronize(t.pin_free[slot]);  // the last copy out of this buffer is done
     if (e != hipSuccess) return e;
-    std::memcpy(t.pin_idx, host, sizeof(int64_t) * (size_t)count);
-    e = hipMemcpyAsync(t.stage_idx, t.pin_idx, sizeof(int64_t) * (size_t)count, hipMemcpyHostToDevice, s);
+    std::memcpy(pin, host, sizeof(int64_t) * (size_t)count);
+    e = hipMemcpyAsync(t.stage_idx, pin, sizeof(int64_t) * (size_t)count, hipMemcpyHostToDevice, s);
     if (e != hipSuccess) return e;
-    return hipEventRecord(t.pin_free, s);
+    return hipEventRecord(t.pin_free[slot], s);
 }
 
 unsigned blocks_for(int64_t n) { return (unsigned)((n + 255) / 256); }
@@ -90,13 +96,15 @@ void free_index_manager(Table& t) {
     (void)hipFree(t.stage_idx);
     (void)hipFree(t.stage_prio);
     if (t.pin_idx) (void)hipHostFree(t.pin_idx);
-    if (t.pin_free) (void)hipEventDestroy(t.pin_free);
+    for (int k = 0; k < kStageSlots; k++) {
+        if (t.pin_free[k]) (void)hipEventDestroy(t.pin_free[k]);
+        t.pin_free[k] = nullptr;
+    }
     t.order = nullptr;
     t.committed = nullptr;
     t.stage_idx = nullptr;
     t.stage_prio = nullptr;
     t.pin_idx = nullptr;
-    t.pin_free = nullptr;
     std::vector<int32_t>().swap(t.free_q);
     std::vector<int32_t>().swap(t.order_h);
     std::vector<uint8_t>().swap(t.slot_state);
@@ -164,13 +172,14 @@ extern "C" int gear_table_use_allocator(gear_table* h, int32_t removal, int64_t 
         (e = hipMalloc(reinterpret_cast<void**>(&t->committed), (size_t)t->N)) != hipSuccess ||
         (e = hipMalloc(reinterpret_cast<void**>(&t->stage_idx), sizeof(int64_t) * gear::kStageRows)) != hipSuccess ||
         (e = hipMalloc(reinterpret_cast<void**>(&t->stage_prio), sizeof(uint32_t) * gear::kStageRows)) != hipSuccess ||
-        (e = hipHostMalloc(reinterpret_cast<void**>(&t->pin_idx), sizeof(int64_t) * gear::kStageRows,
-                           hipHostMallocDefault)) != hipSuccess) {
+        (e = hipHostMalloc(reinterpret_cast<void**>(&t->pin_idx),
+                           sizeof(int64_t) * gear::kStageRows * gear::kStageSlots, hipHostMallocDefault)) != hipSuccess) {
         gear::free_index_manager(*t);
         return fail(GEAR_E_NOMEM, "gear_table_use_allocator: device arrays");
     }
-    if ((e = hipEventCreateWithFlags(&t->pin_free, hipEventDisableTiming)) != hipSuccess ||
-        (e = hipMemset(t->committed, 0, (size_t)t->N)) != hipSuccess ||
+    for (int k = 0; k < gear::kStageSlots && e == hipSuccess; k++)
+        e = hipEventCreateWithFlags(&t->pin_free[k], hipEventDisableTiming);
+    if (e != hipSuccess || (e = hipMemset(t->committed, 0, (size_t)t->N)) != hipSuccess ||
         (e = hipDeviceSynchronize()) != hipSuccess) {
         gear::free_index_manager(*t);
         return hip_fail(e, "gear_table_use_allocator: initialising");

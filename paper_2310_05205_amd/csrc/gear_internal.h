@@ -29,8 +29,11 @@ constexpr int kTopkBins = 4096;       // bins of one TopK digit pass (12-bit dig
 constexpr int kTopkStateWords = 8;
 constexpr int kTopkRankBlock = 512;    // keys one TopK rank workgroup compares against
 constexpr int kTopkMaxK = GEAR_MAX_TOPK;
-// Index manager: index lists move to the device in chunks of this many.
+// Index manager: index lists move to the device in chunks of this many,
+// through a ring of this many pinned host buffers (a buffer is refilled only
+// after the copy out of it has completed).
 constexpr int64_t kStageRows = 1 << 16;
+constexpr int kStageSlots = 4;
 
 // Per-slot state of the index manager (host side).
 enum : uint8_t { kSlotFree = 0, kSlotPending = 1, kSlotCommitted = 2, kSlotMark = 3 };
@@ -83,8 +86,9 @@ struct Table {
     uint8_t* committed = nullptr;     // device [N]: 1 for committed slots
     int64_t* stage_idx = nullptr;     // device staging [kStageRows]
     uint32_t* stage_prio = nullptr;   // device staging [kStageRows]
-    int64_t* pin_idx = nullptr;       // pinned host staging [kStageRows]
-    hipEvent_t pin_free = nullptr;    // recorded after the last copy out of pin_idx
+    int64_t* pin_idx = nullptr;       // pinned host staging [kStageSlots][kStageRows]
+    hipEvent_t pin_free[kStageSlots] = {};  // recorded after the last copy out of each slot
+    int pin_next = 0;                 // slot the next chunk uses
 
     uint64_t* topk_keys = nullptr;    // [kTopkMaxK] selected keys (p << 32 | ~slot), equal priorities in slot order
     uint32_t* topk_rank = nullptr;    // [kTopkMaxK] place of each key in descending order
