@@ -240,12 +240,86 @@ int gear_select(gear_table *t, int32_t strategy, int32_t B, int32_t L, uint64_t 
  *   d_out           host array of ncols device pointers; d_out[j] receives
  *                   B*L*elem_bytes[col_ids[j]] bytes laid out [B][L][elem_bytes]
  *
- * A draw whose index lies outside [0, capacity) or whose start lies outside
- * [0, T-L] gets zero bytes and sets GEAR_STATUS_BAD_INDEX.
+ * Index -1 marks a draw with no trajectory (a missing TopK entry, a draw
+ * another shard owns): its window is zero bytes.  A draw whose index is
+ * otherwise outside [0, capacity), or whose start lies outside [0, T-L],
+ * also gets zero bytes and sets GEAR_STATUS_BAD_INDEX.
  * Errors: GEAR_E_INVAL, GEAR_E_HIP.
  */
 int gear_collect(gear_table *t, const int64_t *d_idx, const int32_t *d_start, int32_t B, int32_t L,
                  const int32_t *col_ids, int32_t ncols, void *const *d_out, void *stream);
+
+/*
+ * Selection over G shards, one GPU's share (Sec. 3.3 centralized and
+ * decentralized selection; Sec. 3.4: global index = shard * capacity +
+ * local index).  Each shard is a table on its own GPU; the exchanges between
+ * the calls (an all-gather of G totals, an all-reduce of B values, a gather
+ * of G*K candidates) are the caller's collectives.
+ */
+
+/*
+ * gear_shard_total - the sum of the table's priorities (uint64), written to
+ * device memory d_total (rescanning first if needed): this shard's entry of
+ * the totals that every shard needs.  Errors: GEAR_E_INVAL, GEAR_E_HIP.
+ */
+int gear_shard_total(gear_table *t, uint64_t *d_total, void *stream);
+
+/*
+ * gear_select_shard - shard g's part of prioritized selection over G shards.
+ * Every shard draws the same numbers r_b in [0, S) with S the sum of
+ * d_totals (device uint64[G], identical on every shard; the sum must fit in
+ * 64 bits) and resolves the draws in [P_g, P_g + S_g), P_g the sum of the
+ * totals before g, exactly as gear_select(GEAR_PRIORITIZED) over the
+ * concatenated shards.
+ *
+ *   base        added to the slot of an owned draw (g * capacity gives global
+ *               indices, 0 local ones)
+ *   d_idx       device int64[B]: slot + base for owned draws, -1 otherwise
+ *   d_start     device int32[B]: window starts of all B draws (the same on
+ *               every shard)
+ *   d_sel_prio  device uint32[B] or NULL: the priority of each owned draw,
+ *               0 otherwise (an all-reduce-max over shards gives every
+ *               shard the full list for gear_is_weights)
+ *
+ * When S is 0 every draw gets -1 and GEAR_STATUS_NO_WEIGHT is set.
+ * Errors: GEAR_E_INVAL, GEAR_E_HIP.
+ */
+int gear_select_shard(gear_table *t, int32_t G, int32_t g, const uint64_t *d_totals, int64_t base, int32_t B,
+                      int32_t L, uint64_t seed, int64_t *d_idx, int32_t *d_start, uint32_t *d_sel_prio,
+                      void *stream);
+
+/*
+ * gear_is_weights - importance-sampling weights (p_min / p_b)^beta of B
+ * selected priorities d_sel_prio (device uint32[B]), p_min the smallest
+ * non-zero one, computed in double and rounded once; 0 where p_b is 0.  The
+ * same weights gear_select returns.  Uses the table's scratch and stream
+ * order.  Errors: GEAR_E_INVAL, GEAR_E_HIP.
+ */
+int gear_is_weights(gear_table *t, const uint32_t *d_sel_prio, int32_t B, float beta, float *d_weights,
+                    void *stream);
+
+/*
+ * gear_topk_merge - the global top-K of G local top-K lists (Sec. 3.3,
+ * decentralized selection: the central GPU computes the global top-K of the
+ * shards' partial results).  Runs on the current HIP device.
+ *
+ *   d_prio, d_gidx  device uint32[G][K] and int64[G][K]: list g is shard g's
+ *                   gear_select(GEAR_TOPK) result as global indices, with
+ *                   the priorities; sorted (priority descending, index
+ *                   ascending), entries with index -1 last
+ *   T, L, seed      as for gear_select: output position b gets the window
+ *                   start drawn for draw b
+ *   d_idx, d_start  device int64[K], int32[K]; positions past the candidates
+ *                   get -1 and 0
+ *   d_weights       device float[K] or NULL: 1, or 0 past the candidates
+ *   d_out_prio      device uint32[K] or NULL: the merged priorities
+ *
+ * Equals gear_select(GEAR_TOPK) over the concatenated shards when the lists
+ * are sorted as stated.  Errors: GEAR_E_INVAL, GEAR_E_HIP.
+ */
+int gear_topk_merge(const uint32_t *d_prio, const int64_t *d_gidx, int32_t G, int32_t K, int32_t T, int32_t L,
+                    uint64_t seed, int64_t *d_idx, int32_t *d_start, float *d_weights, uint32_t *d_out_prio,
+                    void *stream);
 
 /*
  * gear_update_priorities - write new priorities for selected slots (Sec. 3.2:

@@ -292,7 +292,9 @@ int oracle_select(int strategy, const uint32_t *priority, int64_t N,
 /* bytes.  For each draw b and step t < L:                                   */
 /*   out[c][b][t] = column c, block idx[b], step start[b] + t                */
 /* Output per column is contiguous [B][L][elem_bytes[c]].                    */
-/* Returns ORC_INVAL on an out-of-range index or start.                      */
+/* Index -1 marks a draw with no trajectory (a missing TopK entry, a draw    */
+/* owned by another shard): its window is all zeros.  Returns ORC_INVAL on   */
+/* any other out-of-range index, or an out-of-range start.                   */
 /* ------------------------------------------------------------------------ */
 int oracle_collect(int32_t ncols, const uint8_t *const *col_base, const int64_t *elem_bytes,
                    int64_t N, int32_t T, const int64_t *idx, const int32_t *start,
@@ -302,11 +304,15 @@ int oracle_collect(int32_t ncols, const uint8_t *const *col_base, const int64_t 
     if (ncols <= 0 || B <= 0 || L <= 0 || L > T)
         return ORC_INVAL;
     for (b = 0; b < B; b++)
-        if (idx[b] < 0 || idx[b] >= N || start[b] < 0 || start[b] > T - L)
+        if (idx[b] != -1 && (idx[b] < 0 || idx[b] >= N || start[b] < 0 || start[b] > T - L))
             return ORC_INVAL;
     for (c = 0; c < ncols; c++) {
         int64_t E = elem_bytes[c];
         for (b = 0; b < B; b++) {
+            if (idx[b] == -1) {
+                memset(out[c] + (int64_t)b * L * E, 0, (size_t)(L * E));
+                continue;
+            }
             for (t = 0; t < L; t++) {
                 const uint8_t *src = col_base[c] + ((idx[b] * (int64_t)T) + start[b] + t) * E;
                 uint8_t *dst = out[c] + (((int64_t)b * L) + t) * E;

@@ -11,7 +11,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libgear.so")
-SOURCES = ["table.hip", "alloc.hip", "select.hip", "topk.hip", "collect.hip", "update.hip"]
+SOURCES = ["table.hip", "alloc.hip", "select.hip", "topk.hip", "shard.hip", "collect.hip", "update.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -86,11 +86,17 @@ __device__ inline typename Elem<WIDTH>::type zero_elem() {
     return typename Elem<WIDTH>::type(0);
 }
 
-// Validated source byte offset of window b's first step, or -1.
+// Source byte offset of window b's first step; kNoWindow for index -1 (a
+// draw with no trajectory: a missing TopK entry, a draw another shard
+// owns), kBadWindow for an index or start out of range.  Both read as zeros.
+constexpr int64_t kNoWindow = -1;
+constexpr int64_t kBadWindow = -2;
+
 __device__ inline int64_t window_offset(const CollectArgs& a, const ColTask& c, int64_t b) {
     const int64_t i = a.idx[b];
     const int32_t s = a.start[b];
-    if (i < 0 || i >= a.N || s < 0 || s > a.T - a.L) return -1;
+    if (i == -1) return kNoWindow;
+    if (i < 0 || i >= a.N || s < 0 || s > a.T - a.L) return kBadWindow;
     return (i * a.T + s) * c.E;
 }
 
@@ -105,7 +111,7 @@ __device__ void copy_wide(const CollectArgs& a, const ColTask& c, int64_t q) {
     const int64_t so = window_offset(a, c, b);
     if (so < 0) {
         for (int64_t e = threadIdx.x; e < n; e += kThreads) store_stream<WIDTH>(dst + e, zero_elem<WIDTH>());
-        if (threadIdx.x == 0) atomicOr(a.status, GEAR_STATUS_BAD_INDEX);
+        if (threadIdx.x == 0 && so == kBadWindow) atomicOr(a.status, GEAR_STATUS_BAD_INDEX);
         return;
     }
     const V* src = reinterpret_cast<const V*>(c.src + so + off0);
@@ -132,7 +138,7 @@ __device__ void copy_narrow(const CollectArgs& a, const ColTask& c, int64_t q) {
     if ((int)threadIdx.x < nb) {
         const int64_t so = window_offset(a, c, b0 + threadIdx.x);
         s_off[threadIdx.x] = so < 0 ? -1 : so / WIDTH;
-        if (so < 0) s_bad = 1;
+        if (so == kBadWindow) s_bad = 1;
     }
     __syncthreads();
     if (threadIdx.x == 0 && s_bad) atomicOr(a.status, GEAR_STATUS_BAD_INDEX);

@@ -112,8 +112,12 @@ class DeviceGuard {
 
 // Kernel launchers (each returns hipSuccess or the launch error).
 hipError_t launch_scan(Table& t, hipStream_t s);
+// With shard_totals (device uint64[G]), the table is shard g of G: draws are
+// numbers over the sum of all totals, and only those in this shard's range
+// are resolved (slot + base); the rest get slot -1.
 hipError_t launch_search(Table& t, int32_t B, int32_t L, uint64_t seed, bool want_min,
-                         int64_t* idx, int32_t* start, uint32_t* sel_prio, int* grid_out, hipStream_t s);
+                         int64_t* idx, int32_t* start, uint32_t* sel_prio, int* grid_out, hipStream_t s,
+                         const uint64_t* shard_totals = nullptr, int G = 1, int g = 0, int64_t base = 0);
 hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, float* w, hipStream_t s);
 hipError_t launch_topk(Table& t, int32_t K, int32_t L, uint64_t seed, int64_t* idx, int32_t* start, float* w,
                        hipStream_t s);

@@ -130,9 +130,17 @@ __global__ __launch_bounds__(256) void scan_kernel(const uint32_t* __restrict__ 
     }
 }
 
+// One GPU's share of a selection over G shards (the table is shard g).
+// With totals == NULL the table is the whole population.
+struct Shard {
+    const uint64_t* totals;  // the G shard totals, identical on every shard
+    int G, g;
+    int64_t base;            // added to the local slot of an owned draw
+};
+
 __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict__ prio, int64_t N, Levels lv,
                                                      int32_t B, uint64_t span, uint64_t seed, int want_min,
-                                                     uint32_t* __restrict__ wg_min, uint32_t* status,
+                                                     Shard sh, uint32_t* __restrict__ wg_min, uint32_t* status,
                                                      int64_t* __restrict__ idx, int32_t* __restrict__ start,
                                                      uint32_t* __restrict__ sel_prio) {
     __shared__ uint32_t s_min[4];
@@ -146,10 +154,22 @@ __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict_
     load4_u64(lv.level[top], lv.size[top], lane * 4, t0, t1, t2, t3);
     wave_prefix4(t0, t1, t2, t3, tc0, tc1, tc2, tc3);
     const uint64_t S = read_lane(tc3, 63);
+    // Draws are numbers in [0, S_all); this table owns [P, P + S).
+    uint64_t S_all = S, P = 0;
+    if (sh.totals) {
+        uint64_t all = 0, before = 0;
+        for (int h = lane; h < sh.G; h += 64) {
+            const uint64_t x = sh.totals[h];
+            all += x;
+            before += h < sh.g ? x : 0;
+        }
+        S_all = wave_sum(all);
+        P = wave_sum(before);
+    }
     uint32_t my_min = 0xFFFFFFFFu;  // smallest priority this wave selected
 
     for (int64_t b = wave_id; b < B; b += nwaves) {
-        if (S == 0) {
+        if (S_all == 0) {
             if (lane == 0) {
                 idx[b] = -1;
                 start[b] = 0;
@@ -158,7 +178,18 @@ __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict_
             }
             continue;
         }
-        uint64_t r = scale_draw(splitmix64_out(seed, 2 * (uint64_t)b), S);
+        uint64_t r = scale_draw(splitmix64_out(seed, 2 * (uint64_t)b), S_all);
+        if (sh.totals) {
+            if (r < P || r - P >= S) {  // another shard's draw: same window start, no slot
+                if (lane == 0) {
+                    idx[b] = -1;
+                    start[b] = (int32_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b + 1), span);
+                    if (want_min) sel_prio[b] = 0u;
+                }
+                continue;
+            }
+            r -= P;
+        }
         int64_t j = pick_child(tc0, tc1, tc2, tc3, r);
         for (int l = top - 1; l >= 0; l--) {
             uint64_t v0, v1, v2, v3, c0, c1, c2, c3;
@@ -173,7 +204,7 @@ __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict_
         wave_prefix4(p0, p1, p2, p3, c0, c1, c2, c3);
         const int cnt = pick_child(c0, c1, c2, c3, r);
         if (lane == 0) {
-            idx[b] = j * kTile + cnt;
+            idx[b] = sh.base + j * kTile + cnt;
             start[b] = (int32_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b + 1), span);
         }
         if (want_min) {
@@ -288,11 +319,18 @@ hipError_t launch_scan(Table& t, hipStream_t s) {
 }
 
 hipError_t launch_search(Table& t, int32_t B, int32_t L, uint64_t seed, bool want_min, int64_t* idx,
-                         int32_t* start, uint32_t* sel_prio, int* grid_out, hipStream_t s) {
-    int64_t g = ((int64_t)B + 3) / 4;  // one wave per draw while the grid allows
-    const int grid = (int)(g < kSearchMaxGrid ? g : kSearchMaxGrid);
+                         int32_t* start, uint32_t* sel_prio, int* grid_out, hipStream_t s,
+                         const uint64_t* shard_totals, int G, int g, int64_t base) {
+    int64_t gw = ((int64_t)B + 3) / 4;  // one wave per draw while the grid allows
+    const int grid = (int)(gw < kSearchMaxGrid ? gw : kSearchMaxGrid);
+    Shard sh;
+    sh.totals = shard_totals;
+    sh.G = G;
+    sh.g = g;
+    sh.base = base;
     hipLaunchKernelGGL(search_kernel, dim3(grid), dim3(256), 0, s, t.priority, t.N, tree(t), B,
-                       (uint64_t)(t.T - L + 1), seed, want_min ? 1 : 0, t.wg_min, t.status, idx, start, sel_prio);
+                       (uint64_t)(t.T - L + 1), seed, want_min ? 1 : 0, sh, t.wg_min, t.status, idx, start,
+                       sel_prio);
     *grid_out = grid;
     return hipGetLastError();
 }

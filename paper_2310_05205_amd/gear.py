@@ -68,10 +68,15 @@ def lib():
         L.gear_commit.argtypes = [vp, i64, vp, vp, vp]
         pi64 = ctypes.POINTER(i64)
         L.gear_allocator_info.argtypes = [vp, pi64, pi64, pi64]
+        L.gear_shard_total.argtypes = [vp, vp, vp]
+        L.gear_select_shard.argtypes = [vp, i32, i32, vp, i64, i32, i32, u64, vp, vp, vp, vp]
+        L.gear_is_weights.argtypes = [vp, vp, i32, ctypes.c_float, vp, vp]
+        L.gear_topk_merge.argtypes = [vp, vp, i32, i32, i32, i32, u64, vp, vp, vp, vp, vp]
         for name in ["gear_table_create", "gear_table_destroy", "gear_insert", "gear_select", "gear_collect",
                      "gear_update_priorities", "gear_table_sync", "gear_table_info", "gear_table_column",
                      "gear_table_priorities", "gear_table_set_options", "gear_table_use_allocator",
-                     "gear_allocate", "gear_commit", "gear_allocator_info"]:
+                     "gear_allocate", "gear_commit", "gear_allocator_info", "gear_shard_total",
+                     "gear_select_shard", "gear_is_weights", "gear_topk_merge"]:
             getattr(L, name).restype = ctypes.c_int
         L.gear_last_error.argtypes = []
         L.gear_last_error.restype = ctypes.c_char_p
@@ -185,6 +190,42 @@ def gear_allocator_info(table):
     return c.value, p.value, f.value
 
 
+def gear_shard_total(table, d_total, stream=0):
+    _check(lib().gear_shard_total(table, d_total, stream))
+
+
+def gear_select_shard(table, G, g, d_totals, base, B, L, seed, d_idx, d_start, d_sel_prio=0, stream=0):
+    _check(lib().gear_select_shard(table, int(G), int(g), d_totals, int(base), int(B), int(L),
+                                   int(seed) & ((1 << 64) - 1), d_idx, d_start, d_sel_prio or None, stream))
+
+
+def gear_is_weights(table, d_sel_prio, B, beta, d_weights, stream=0):
+    _check(lib().gear_is_weights(table, d_sel_prio, int(B), ctypes.c_float(beta), d_weights, stream))
+
+
+def gear_topk_merge(d_prio, d_gidx, G, K, T, L, seed, d_idx, d_start, d_weights=0, d_out_prio=0, stream=0):
+    _check(lib().gear_topk_merge(d_prio, d_gidx, int(G), int(K), int(T), int(L), int(seed) & ((1 << 64) - 1),
+                                 d_idx, d_start, d_weights or None, d_out_prio or None, stream))
+
+
+def topk_merge(prio, gidx, K, T, L, seed, device=0):
+    """Global top-K of G sorted local top-K lists (torch tensors [G, K] of
+    uint32-valued priorities and int64 global indices on `device`).
+    Returns (idx, start, weights, priorities)."""
+    import torch
+    dev = torch.device("cuda", device)
+    G = int(gidx.shape[0])
+    idx = torch.empty(K, dtype=torch.int64, device=dev)
+    start = torch.empty(K, dtype=torch.int32, device=dev)
+    w = torch.empty(K, dtype=torch.float32, device=dev)
+    p = torch.empty(K, dtype=torch.int32, device=dev)
+    prio = prio.contiguous()
+    gidx = gidx.contiguous()
+    gear_topk_merge(prio.data_ptr(), gidx.data_ptr(), G, K, T, L, seed, idx.data_ptr(), start.data_ptr(),
+                    w.data_ptr(), p.data_ptr(), torch.cuda.current_stream(dev).cuda_stream)
+    return idx, start, w, p
+
+
 class _DeviceBytes:
     """Describes device memory to torch.as_tensor (array-interface protocol)."""
 
@@ -274,6 +315,29 @@ class Table:
 
     def allocator_info(self):
         return gear_allocator_info(self.handle)
+
+    def shard_total(self, out, stream=None):
+        """Writes this table's priority total into `out` (a one-element int64
+        or uint64-sized device tensor view)."""
+        gear_shard_total(self.handle, out.data_ptr(), self._stream(stream))
+
+    def select_shard(self, G, g, totals, base, B, L, seed, stream=None):
+        """Shard g's part of prioritized selection; returns (idx, start, sel_prio)."""
+        torch = self._torch
+        dev = torch.device("cuda", self.device)
+        idx = torch.empty(B, dtype=torch.int64, device=dev)
+        start = torch.empty(B, dtype=torch.int32, device=dev)
+        p = torch.empty(B, dtype=torch.int32, device=dev)
+        gear_select_shard(self.handle, G, g, totals.data_ptr(), base, B, L, seed, idx.data_ptr(), start.data_ptr(),
+                          p.data_ptr(), self._stream(stream))
+        return idx, start, p
+
+    def is_weights(self, sel_prio, beta, stream=None):
+        torch = self._torch
+        w = torch.empty(int(sel_prio.shape[0]), dtype=torch.float32, device=torch.device("cuda", self.device))
+        gear_is_weights(self.handle, sel_prio.data_ptr(), int(sel_prio.shape[0]), beta, w.data_ptr(),
+                        self._stream(stream))
+        return w
 
     def column_view(self, c):
         """Column c's blocks in place, [capacity, T*E_c] bytes: a torch uint8

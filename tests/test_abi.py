@@ -58,6 +58,11 @@ def test_argument_validation_without_device():
     assert lib.gear_allocate(None, 1, None, None) == gear.GEAR_E_INVAL
     assert lib.gear_commit(None, 1, None, None, None) == gear.GEAR_E_INVAL
     assert lib.gear_allocator_info(None, None, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_shard_total(None, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_select_shard(None, 1, 0, None, 0, 1, 1, 0, None, None, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_is_weights(None, None, 1, ctypes.c_float(0), None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_topk_merge(None, None, 0, 1, 1, 1, 0, None, None, None, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_topk_merge(None, None, 2, 1, 1, 1, 0, None, None, None, None, None) == gear.GEAR_E_INVAL
     with pytest.raises(gear.GearError) as e:
         gear.gear_table_create([4], 16, 0)
     assert e.value.code == gear.GEAR_E_INVAL

@@ -56,9 +56,17 @@ def test_collect_several_columns_and_stamps():
 def test_collect_rejects_out_of_range():
     tab = np.zeros((4, 10), dtype=np.uint8)
     assert oracle.collect([tab], 10, [4], [0], 3)[0] == oracle.INVAL
-    assert oracle.collect([tab], 10, [-1], [0], 3)[0] == oracle.INVAL
+    assert oracle.collect([tab], 10, [-2], [0], 3)[0] == oracle.INVAL
     assert oracle.collect([tab], 10, [1], [8], 3)[0] == oracle.INVAL
     assert oracle.collect([tab], 10, [1], [7], 3)[0] == oracle.OK
+
+
+def test_collect_index_minus_one_is_an_empty_window():
+    # -1 marks a draw with no trajectory: its window is zeros, whatever start.
+    tab = np.arange(40, dtype=np.uint8).reshape(4, 10) + 1
+    st, outs = oracle.collect([tab], 10, [2, -1, 0], [1, 99, 7], 3)
+    assert st == oracle.OK
+    np.testing.assert_array_equal(outs[0], [[22, 23, 24], [0, 0, 0], [8, 9, 10]])
 
 
 def test_update_last_occurrence_wins():

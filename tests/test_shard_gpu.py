@@ -1,0 +1,155 @@
+"""GPU checks of one GPU's share of selection over G shards (GEAR Sec. 3.3;
+Sec. 3.4 global index = shard * capacity + local index).  G tables on one
+GPU stand in for the G shards; the exchanges between the calls are done
+here with torch.  The pin is the oracle's selection over the concatenated
+priorities: the shards' answers together must equal it bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import gen
+import oracle
+from paper_2310_05205_amd import gear
+from tests.helpers import DEV, cuda, host, say
+
+pytestmark = pytest.mark.gpu
+
+U = gen.PrioDist(gen.PRIO_UNIFORM, 1, 1000)
+PARETO = gen.PrioDist(gen.PRIO_PARETO, 1.5, float(1 << 24))
+STAMP = gen.Column("stamp", gen.STAMP, 1)
+
+
+def _shards(G, cap, dists, T=4, cols=()):
+    """G ring tables, shard g holding global slots [g*cap, (g+1)*cap); a None
+    distribution gives a shard of zero priorities.  Returns (tables, priorities
+    of the concatenation)."""
+    tabs, allp = [], []
+    for g in range(G):
+        d = dists[g % len(dists)]
+        p = np.zeros(cap, np.uint32) if d is None else gen.insert_priorities(d, 100 + g, 0, cap)
+        t = gear.Table([c.elem_bytes for c in cols], cap, T, gear.GEAR_DEVICE, DEV)
+        rows = [gen.fill_rows_cpu(c, 0, 0, T, g * cap, cap) for c in cols]
+        t.insert(rows, p)
+        tabs.append(t)
+        allp.append(p)
+    return tabs, np.concatenate(allp)
+
+
+def _totals(tabs):
+    totals = torch.zeros(len(tabs), dtype=torch.int64, device=cuda())
+    for g, t in enumerate(tabs):
+        t.shard_total(totals[g:g + 1])
+    return totals
+
+
+CASES = [(1, 5000, [U]), (3, 4096, [U]), (8, 3000, [PARETO, U]), (4, 70000, [PARETO]),
+         (5, 2000, [U, None]), (2, (1 << 20) + 77, [PARETO])]
+
+
+@pytest.mark.parametrize("G,cap,dists", CASES, ids=["G1", "G3", "G8-mixed", "G4-70k", "G5-zero-shards", "G2-1M"])
+def test_sharded_prioritized_equals_concatenated(G, cap, dists):
+    tabs, P = _shards(G, cap, dists)
+    try:
+        totals = _totals(tabs)
+        np.testing.assert_array_equal(host(totals).astype(np.uint64),
+                                      P.reshape(G, cap).astype(np.uint64).sum(axis=1))
+        for it, (B, L, beta) in enumerate([(8192, 2, 0.4), (1000, 4, 1.0), (12000, 1, 0.0)]):
+            say("shards G=%d cap=%d draw set %d" % (G, cap, it))
+            seed = gen.select_seed(21, it)
+            st, oidx, ostart, ow = oracle.select(oracle.PRIORITIZED, P, G * cap, 4, B, L, seed, beta, True)
+            assert st == oracle.OK
+            parts = [t.select_shard(G, g, totals, g * cap, B, L, seed) for g, t in enumerate(tabs)]
+            idx = torch.stack([p[0] for p in parts])
+            owners = (idx >= 0).sum(dim=0)
+            assert int(owners.min()) == 1 and int(owners.max()) == 1     # every draw owned once
+            np.testing.assert_array_equal(host(idx.max(dim=0).values), oidx)
+            for p in parts:
+                np.testing.assert_array_equal(host(p[1]), ostart)        # same starts everywhere
+            sel = torch.stack([p[2] for p in parts]).max(dim=0).values  # the all-reduce of priorities
+            np.testing.assert_array_equal(host(sel).astype(np.uint32), P[oidx])
+            w = tabs[0].is_weights(sel, beta)
+            np.testing.assert_allclose(host(w).astype(np.float64), ow.astype(np.float64), rtol=1e-6, atol=0)
+        for t in tabs:
+            assert t.sync() == 0
+    finally:
+        for t in tabs:
+            t.close()
+
+
+def test_all_shards_empty_sets_no_weight():
+    tabs, P = _shards(3, 100, [None])
+    try:
+        totals = _totals(tabs)
+        for g, t in enumerate(tabs):
+            idx, start, p = t.select_shard(3, g, totals, g * 100, 50, 1, 5)
+            assert np.all(host(idx) == -1) and np.all(host(p) == 0)
+            assert t.sync() == gear.GEAR_STATUS_NO_WEIGHT
+    finally:
+        for t in tabs:
+            t.close()
+
+
+TOPK_CASES = [(1, 5000, [PARETO], 777), (4, 20000, [PARETO], 8192), (8, 3000, [U, None], 5000),
+              (3, 100, [U], 1000), (6, 50000, [gen.PrioDist(gen.PRIO_UNIFORM, 1, 3)], 16384)]
+
+
+@pytest.mark.parametrize("G,cap,dists,K", TOPK_CASES, ids=["G1", "G4-pareto", "G8-zero-shards", "G3-short", "G6-ties"])
+def test_topk_merge_equals_concatenated(G, cap, dists, K):
+    T, L = 5, 2
+    tabs, P = _shards(G, cap, dists, T=T)
+    try:
+        for it in range(2):
+            say("topk merge G=%d cap=%d K=%d iteration %d" % (G, cap, K, it))
+            seed = gen.select_seed(31, it)
+            pr = np.zeros((G, K), np.uint32)
+            gi = np.full((G, K), -1, np.int64)
+            for g, t in enumerate(tabs):
+                local, _, _ = t.select(gear.GEAR_TOPK, K, L, 1234 + g)       # each shard's own draw seed
+                local = host(local)
+                ok = local >= 0
+                gi[g, ok] = g * cap + local[ok]
+                pr[g, ok] = P[g * cap + local[ok]]
+                t.sync()
+            idx, start, w, p = gear.topk_merge(torch.from_numpy(pr.view(np.int32)).to(cuda()),
+                                               torch.from_numpy(gi).to(cuda()), K, T, L, seed, DEV)
+            st, oidx, ostart, ow = oracle.select(oracle.TOPK, P, G * cap, T, K, L, seed, 0.0, True)
+            np.testing.assert_array_equal(host(idx), oidx)
+            np.testing.assert_array_equal(host(start), ostart)
+            np.testing.assert_array_equal(host(w), ow)
+            np.testing.assert_array_equal(host(p).view(np.uint32)[oidx >= 0], P[oidx[oidx >= 0]])
+            # The next round sees new priorities on the selected slots.
+            for g, t in enumerate(tabs):
+                mine = oidx[(oidx >= g * cap) & (oidx < (g + 1) * cap)] - g * cap
+                if mine.size:
+                    newp = (P[g * cap + mine] // 2).astype(np.uint32)
+                    t.update_priorities(torch.from_numpy(mine).to(cuda()), torch.from_numpy(newp).to(cuda()))
+                    P[g * cap + mine] = newp
+    finally:
+        for t in tabs:
+            t.close()
+
+
+def test_collect_skips_other_shards_draws():
+    # Each shard collects the windows of its own draws; index -1 (another
+    # shard's draw) reads as zeros and is not an error.
+    G, cap, T, L = 3, 500, 6, 3
+    tabs, P = _shards(G, cap, [U], T=T, cols=(STAMP,))
+    try:
+        totals = _totals(tabs)
+        B = 300
+        seed = gen.select_seed(41, 0)
+        st, oidx, ostart, _ = oracle.select(oracle.PRIORITIZED, P, G * cap, T, B, L, seed, 0.0, False)
+        rows = gen.fill_rows_cpu(STAMP, 0, 0, T, 0, G * cap)
+        for g, t in enumerate(tabs):
+            idx, start, _ = t.select_shard(G, g, totals, 0, B, L, seed)   # local indices
+            out = host(t.collect(idx, start, L)[0])
+            mine = (oidx >= g * cap) & (oidx < (g + 1) * cap)
+            expect = np.zeros((B, L * STAMP.elem_bytes), np.uint8)
+            st2, o = oracle.collect([rows], T, oidx[mine], ostart[mine], L)
+            expect[mine] = o[0]
+            np.testing.assert_array_equal(out, expect)
+            assert t.sync() == 0
+    finally:
+        for t in tabs:
+            t.close()
