@@ -15,6 +15,7 @@ sample of the same workload.
 
   python bench.py [--steps K] [--warmup W] [--workload mat|gato-host|dt|tiny|select-stress|topk]
   python bench.py --workload mat-insert   # insertion through the index manager (own metric)
+  python bench.py --workload shard-select # one GPU's share of selection over 8 shards (own metric)
   python bench.py --calibrate     # plain copy kernel of known size, for counter scaling
   python bench.py --ceilings      # HBM read / write / copy rates of plain kernels
 """
@@ -82,7 +83,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="mat",
-                    choices=["mat", "gato-host", "dt", "tiny", "select-stress", "topk", "mat-insert"])
+                    choices=["mat", "gato-host", "dt", "tiny", "select-stress", "topk", "mat-insert", "shard-select"])
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
     ap.add_argument("--incremental", action="store_true",
                     help="keep the selection sum tree current across updates (no rescan per step)")
@@ -322,6 +323,89 @@ def run_insert(args):
     print(json.dumps(line), flush=True)
 
 
+def run_shard(args):
+    """One GPU's share of selection over G = 8 shards, each shaped like the
+    MAT priorities (500000 log-normal priorities; the other shards' totals
+    are taken equal to this one's).  Times, per call: the shard total, the
+    shard's prioritized select of B = 8192 draws, IS weights over the
+    all-reduced priorities, and the merge of 8 sorted top-8192 lists; plus a
+    plain prioritized select of the same table.  Prints one JSON line."""
+    import numpy as np
+    import torch
+
+    import gen
+    from gen import configs
+    from paper_2310_05205_amd import gear
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    w = configs.MAT
+    G, g, B, K = 8, 3, w.B, 8192
+    dev = torch.device("cuda", 0)
+    sh = torch.cuda.current_stream(dev).cuda_stream
+    t = gear.Table([], w.N, 1, gear.GEAR_DEVICE, 0)   # priorities only: windows of one step
+    t.insert([], gen.insert_priorities(w.prio, w.seed, 0, w.N))
+    totals = torch.zeros(G, dtype=torch.int64, device=dev)
+    t.shard_total(totals[g:g + 1])
+    torch.cuda.synchronize()
+    totals.fill_(int(totals[g].item()))
+    local, _, _ = t.select(gear.GEAR_TOPK, K, 1, 0)
+    lp = torch.from_numpy(t.priorities().view(np.int32)).to(dev)[local]
+    gidx = torch.stack([local + h * w.N for h in range(G)])
+    gprio = torch.stack([lp for _ in range(G)])
+    idx = torch.empty(B, dtype=torch.int64, device=dev)
+    start = torch.empty(B, dtype=torch.int32, device=dev)
+    selp = torch.empty(B, dtype=torch.int32, device=dev)
+    wts = torch.empty(B, dtype=torch.float32, device=dev)
+    midx = torch.empty(K, dtype=torch.int64, device=dev)
+    mstart = torch.empty(K, dtype=torch.int32, device=dev)
+    hev = HipEvents()
+    K_, W = args.steps, args.warmup
+
+    def timed(fn):
+        for i in range(W):
+            fn(i)
+        torch.cuda.synchronize()
+        a, b = hev.create(), hev.create()
+        hev.record(a, sh)
+        for i in range(K_):
+            fn(W + i)
+        hev.record(b, sh)
+        torch.cuda.synchronize()
+        return hev.elapsed_ms(a, b) * 1e3 / K_
+
+    out = {
+        "shard_total_us": timed(lambda i: gear.gear_shard_total(t.handle, totals[g:g + 1].data_ptr(), sh)),
+        "select_shard_us": timed(lambda i: gear.gear_select_shard(t.handle, G, g, totals.data_ptr(), g * w.N, B, 1,
+                                                                  gen.select_seed(w.seed, i), idx.data_ptr(),
+                                                                  start.data_ptr(), selp.data_ptr(), sh)),
+        "is_weights_us": timed(lambda i: gear.gear_is_weights(t.handle, selp.data_ptr(), B, w.beta, wts.data_ptr(), sh)),
+        "topk_merge_us": timed(lambda i: gear.gear_topk_merge(gprio.data_ptr(), gidx.data_ptr(), G, K, w.T, w.L,
+                                                              gen.select_seed(w.seed, i), midx.data_ptr(),
+                                                              mstart.data_ptr(), 0, 0, sh)),
+        "plain_select_us": timed(lambda i: gear.gear_select(t.handle, gear.GEAR_PRIORITIZED, B, 1,
+                                                            gen.select_seed(w.seed, i), w.beta, idx.data_ptr(),
+                                                            start.data_ptr(), wts.data_ptr(), sh)),
+    }
+    if t.sync() != 0:
+        raise SystemExit("device status set during the shard steps")
+    hev.close()
+    t.close()
+    line = {
+        "metric": "sharded selection, one GPU's share: draws resolved per second by this shard",
+        "value": round(B / (out["select_shard_us"] * 1e-6), 1), "unit": "draws/s", "n_gpus": 1, "steps": K_,
+        "warmup": W, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u64",
+        "data": "synthetic",
+        "config": {"workload": "shard-select G=8 shards of N=500000 log-normal priorities, B=8192, TopK K=8192",
+                   "G": G, "g": g, "N_per_shard": w.N, "B": B, "K": K, "parallelism": "1 GPU (shard 3 of 8)"},
+        "per_call_us": {k: round(v, 2) for k, v in out.items()},
+        "note": "the all-gather of 8 totals, the all-reduce of B priorities and the gather of 8 top-K lists "
+                "are the caller's collectives and are not timed here; select_shard rescans only when dirty",
+        "roofline": None, "cpu_baseline": None,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -337,6 +421,9 @@ def main():
         return
     if args.workload == "mat-insert":
         run_insert(args)
+        return
+    if args.workload == "shard-select":
+        run_shard(args)
         return
 
     import numpy as np
