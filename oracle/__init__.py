@@ -60,7 +60,7 @@ def lib():
         L.oracle_prefix_sum.argtypes = [vp, i64, vp]; L.oracle_prefix_sum.restype = u64
         L.oracle_upper_bound.argtypes = [vp, i64, u64]; L.oracle_upper_bound.restype = i64
         L.oracle_select.argtypes = [ctypes.c_int, vp, i64, u64, vp, i64, i32, i32, i32, u64, ctypes.c_float,
-                                    vp, vp, vp, vp]
+                                    ctypes.c_int, vp, vp, vp, vp]
         L.oracle_select.restype = ctypes.c_int
         L.oracle_collect.argtypes = [i32, vp, vp, i64, i32, vp, vp, i32, i32, vp]
         L.oracle_collect.restype = ctypes.c_int
@@ -110,10 +110,12 @@ def upper_bound(C, r):
     return lib().oracle_upper_bound(_ptr(C), C.size, r)
 
 
-def select(strategy, priority, next_seq, T, B, L, seed, beta=0.0, weights=False, order=None):
+def select(strategy, priority, next_seq, T, B, L, seed, beta=0.0, weights=False, order=None, global_min=False):
     """Returns (status, idx int64[B], start int32[B], w float32[B] or None).
     `order`: the committed slots of an index manager, oldest first (FIFO,
-    LIFO and uniform pick from it); None for the ring state `next_seq`."""
+    LIFO and uniform pick from it); None for the ring state `next_seq`.
+    `global_min`: IS weights normalised over every non-zero priority instead
+    of the batch."""
     priority = np.ascontiguousarray(priority, dtype=np.uint32)
     N = priority.size
     idx = np.zeros(max(B, 0), dtype=np.int64)
@@ -127,7 +129,7 @@ def select(strategy, priority, next_seq, T, B, L, seed, beta=0.0, weights=False,
     else:
         optr, nord = None, 0
     st = lib().oracle_select(strategy, _ptr(priority), N, next_seq, optr, nord, T, B, L, seed,
-                             ctypes.c_float(beta), _ptr(idx), _ptr(start), _ptr(w), _ptr(C))
+                             ctypes.c_float(beta), 1 if global_min else 0, _ptr(idx), _ptr(start), _ptr(w), _ptr(C))
     return st, idx, start, w
 
 
@@ -271,9 +273,9 @@ class Store:
         self.next_seq = lib().oracle_insert(len(self.cols), bases, _ptr(Ea), self.N, self.T,
                                             self.next_seq, n, srcs, _ptr(self.priority), _ptr(prio))
 
-    def select(self, strategy, B, L, seed, beta=0.0, weights=False):
+    def select(self, strategy, B, L, seed, beta=0.0, weights=False, global_min=False):
         order = self.im.order() if self.im is not None else None
-        return select(strategy, self.priority, self.next_seq, self.T, B, L, seed, beta, weights, order)
+        return select(strategy, self.priority, self.next_seq, self.T, B, L, seed, beta, weights, order, global_min)
 
     def collect(self, idx, start, L, col_ids=None):
         cols = self.cols if col_ids is None else [self.cols[i] for i in col_ids]

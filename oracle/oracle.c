@@ -174,10 +174,16 @@ static int orc_topk_cmp(const void *a, const void *b)
 /* commit first, and n = norder; FIFO, LIFO and uniform then pick from that  */
 /* list.  With order == NULL the ring state above applies.                   */
 /* ------------------------------------------------------------------------ */
+/*                                                                          */
+/* IS weights normalise by the largest weight: of the batch (global_min = 0, */
+/* the reading used by default), or of every live trajectory with non-zero   */
+/* priority (global_min = 1, the variant of prioritized replay that divides  */
+/* by the largest weight in the whole buffer).                               */
+/* ------------------------------------------------------------------------ */
 int oracle_select(int strategy, const uint32_t *priority, int64_t N,
                   uint64_t next_seq, const int64_t *order, int64_t norder,
                   int32_t T, int32_t B, int32_t L,
-                  uint64_t seed, float beta,
+                  uint64_t seed, float beta, int global_min,
                   int64_t *idx, int32_t *start, float *w,
                   uint64_t *C_scratch /* N entries, prioritized only */)
 {
@@ -260,13 +266,26 @@ int oracle_select(int strategy, const uint32_t *priority, int64_t N,
         }
         if (w != NULL) {
             /* x_b = n * P(idx_b) with P(i) = p_i / S; w'_b = x_b^-beta;
-             * w_b = w'_b / max over the batch of w'. */
+             * w_b = w'_b / max of w' over the batch, or over every slot
+             * with non-zero priority (every such slot is live). */
             double wmax = 0.0;
-            for (b = 0; b < B; b++) {
-                double x = (double)n * (double)priority[idx[b]] / (double)S;
-                double v = pow(x, -(double)beta);
-                if (v > wmax)
-                    wmax = v;
+            if (global_min) {
+                int64_t i;
+                for (i = 0; i < N; i++) {
+                    if (priority[i] > 0) {
+                        double x = (double)n * (double)priority[i] / (double)S;
+                        double v = pow(x, -(double)beta);
+                        if (v > wmax)
+                            wmax = v;
+                    }
+                }
+            } else {
+                for (b = 0; b < B; b++) {
+                    double x = (double)n * (double)priority[idx[b]] / (double)S;
+                    double v = pow(x, -(double)beta);
+                    if (v > wmax)
+                        wmax = v;
+                }
             }
             for (b = 0; b < B; b++) {
                 double x = (double)n * (double)priority[idx[b]] / (double)S;

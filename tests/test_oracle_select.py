@@ -101,6 +101,27 @@ def test_is_weights_closed_form():
         assert w[np.argmin(pb)] == 1.0
 
 
+def test_is_weights_global_minimum_closed_form():
+    # Normalised by the largest weight of any selectable slot, i.e. at the
+    # smallest non-zero priority of the whole table: (p_min_all / p_b)^beta.
+    rng = np.random.default_rng(19)
+    N = 3000
+    p = rng.integers(50, 1 << 20, size=N).astype(np.uint32)
+    p[rng.integers(0, N, size=300)] = 0
+    p[1234] = 7                                     # the global minimum, rarely drawn
+    for beta in [0.0, 0.4, 1.0]:
+        st, idx, start, w = oracle.select(oracle.PRIORITIZED, p, N, 1, 500, 1, 8, beta, True, global_min=True)
+        assert st == oracle.OK
+        closed = (7.0 / p[idx].astype(np.float64)) ** beta
+        np.testing.assert_allclose(w.astype(np.float64), closed, rtol=1e-6, atol=0)
+        assert np.all(w <= 1.0)
+    # When the batch holds the global minimum both normalisations agree.
+    q = np.array([3, 3, 3, 3], dtype=np.uint32)
+    a = oracle.select(oracle.PRIORITIZED, q, 4, 1, 64, 1, 2, 0.6, True)[3]
+    b = oracle.select(oracle.PRIORITIZED, q, 4, 1, 64, 1, 2, 0.6, True, global_min=True)[3]
+    np.testing.assert_array_equal(a, b)
+
+
 def test_is_weights_use_live_count_and_total():
     # With one live trajectory per distinct priority the max weight belongs
     # to the smallest priority and n, S cancel: w = (p_min/p_b)^beta.
