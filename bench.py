@@ -87,6 +87,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
     ap.add_argument("--incremental", action="store_true",
                     help="keep the selection sum tree current across updates (no rescan per step)")
+    ap.add_argument("--global-min", action="store_true",
+                    help="IS weights normalised over the whole table (GEAR_OPT_IS_GLOBAL_MIN)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target oracle time for the CPU baseline")
     ap.add_argument("--calibrate", action="store_true", help="run a plain copy kernel of known size and exit")
     ap.add_argument("--ceilings", action="store_true", help="measure plain read/write/copy HBM rates and exit")
@@ -168,7 +170,7 @@ def profiled_traffic(kernel_key, workload_name):
         return None
 
 
-def cpu_baseline(w, target_s):
+def cpu_baseline(w, target_s, global_min=False):
     """The oracle, single-threaded, on a bounded sample: repeated steps of
     the same workload (select over all N priorities, IS weights, collection
     of the B selected windows, update), collecting from a compact host table
@@ -182,7 +184,7 @@ def cpu_baseline(w, target_s):
     p, next_seq = oracle_priorities(w)
     seed = gen.select_seed(w.seed, 0)
     strat = w.strategies[0]
-    st, idx, start, _ = oracle.select(strat, p, next_seq, w.T, w.B, w.L, seed, w.beta, True)
+    st, idx, start, _ = oracle.select(strat, p, next_seq, w.T, w.B, w.L, seed, w.beta, True, global_min=global_min)
     assert st == oracle.OK
     ks = gen.slot_insertion(idx, next_seq, w.N)
     rows = [gen.fill_rows_list_cpu(c, ci, w.seed, w.T, ks) for ci, c in enumerate(w.columns)]
@@ -191,7 +193,8 @@ def cpu_baseline(w, target_s):
     reps = 0
     t0 = time.perf_counter()
     while True:
-        st, oidx, ostart, ow = oracle.select(strat, p, next_seq, w.T, w.B, w.L, seed, w.beta, True)
+        st, oidx, ostart, ow = oracle.select(strat, p, next_seq, w.T, w.B, w.L, seed, w.beta, True,
+                                             global_min=global_min)
         if rows:
             st2, outs = oracle.collect(rows, w.T, local, ostart, w.L)
             del outs
@@ -444,8 +447,10 @@ def main():
     host_table = w.host_table
     t = gear.Table(w.elem_bytes, w.N, w.T, gear.GEAR_HOST_PINNED if host_table else gear.GEAR_DEVICE, 0)
     fill_table(w, lambda n, ptrs, prio: t.insert(ptrs, prio), device=0)
-    if args.incremental:
-        t.set_options(gear.GEAR_OPT_INCREMENTAL_TREE)
+    opts = (gear.GEAR_OPT_INCREMENTAL_TREE if args.incremental else 0) | \
+        (gear.GEAR_OPT_IS_GLOBAL_MIN if args.global_min else 0)
+    if opts:
+        t.set_options(opts)
 
     K, W = args.steps, args.warmup
     B, L = w.B, w.L
@@ -536,7 +541,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, args.cpu_seconds)
+        cpu = cpu_baseline(w, args.cpu_seconds, args.global_min)
 
     steps_per_s = B * L * K / wall
     line = {
@@ -549,7 +554,8 @@ def main():
                    "residency": "pinned-host" if host_table else "hbm",
                    "strategy": {0: "fifo", 1: "lifo", 2: "uniform", 3: "prioritized", 4: "topk"}[strategy],
                    "is_weights": bool(w.weights), "parallelism": "1 GPU",
-                   "tree": "incremental" if args.incremental else "rescan per select"},
+                   "tree": "incremental" if args.incremental and not args.global_min else "rescan per select",
+                   "is_normalisation": "table minimum" if args.global_min else "batch minimum"},
         "roofline": roof,
         "cpu_baseline": cpu,
         "stages_ms": {"select": round(sel_ms, 5), "collect": round(col_ms, 5), "update": round(upd_ms, 5),

@@ -63,6 +63,10 @@ extern "C" {
 
 /* Table options (gear_table_set_options). */
 #define GEAR_OPT_INCREMENTAL_TREE 1u  /* updates maintain the selection sum tree in place */
+#define GEAR_OPT_IS_GLOBAL_MIN    2u  /* IS weights (p_min / p_b)^beta with p_min the smallest
+                                         non-zero priority of the whole table, not of the
+                                         batch (every select after a change rescans; updates
+                                         then do not maintain the tree) */
 
 /* Limits. */
 #define GEAR_MAX_CAPACITY  (1ll << 30)  /* keeps every priority total below 2^62 */
@@ -339,6 +343,14 @@ int gear_topk_merge(const uint32_t *d_prio, const int64_t *d_gidx, int32_t G, in
  */
 int gear_update_priorities(gear_table *t, const int64_t *d_idx, const uint32_t *d_new_priorities,
                            int32_t B, void *stream);
+
+/*
+ * gear_table_set_options - set the table's GEAR_OPT_* bits (replacing the
+ * previous set).  Takes effect for the next calls; switching
+ * GEAR_OPT_IS_GLOBAL_MIN on makes the next prioritized select rescan.
+ * Errors: GEAR_E_INVAL (NULL table, unknown bits).
+ */
+int gear_table_set_options(gear_table *t, uint32_t options);
 
 /*
  * gear_table_sync - wait for `stream`, then read and clear the device status

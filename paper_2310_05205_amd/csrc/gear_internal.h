@@ -62,6 +62,7 @@ struct Table {
                                       // one and zeroes the other for the next scan
     int tree_parity = 0;              // copy filled by the last scan
     uint32_t* wg_min = nullptr;       // [kSearchMaxGrid] per-workgroup minimum selected priority
+    uint32_t* chunk_min = nullptr;    // [nchunks] smallest non-zero priority of each scan chunk
     uint32_t* status = nullptr;       // device status word
     bool cdf_dirty = true;            // the tree does not reflect the priorities
     uint32_t options = 0;             // GEAR_OPT_* bits
@@ -118,7 +119,8 @@ hipError_t launch_scan(Table& t, hipStream_t s);
 hipError_t launch_search(Table& t, int32_t B, int32_t L, uint64_t seed, bool want_min,
                          int64_t* idx, int32_t* start, uint32_t* sel_prio, int* grid_out, hipStream_t s,
                          const uint64_t* shard_totals = nullptr, int G = 1, int g = 0, int64_t base = 0);
-hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, float* w, hipStream_t s);
+hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, float* w, hipStream_t s,
+                             bool global_min = false);
 hipError_t launch_topk(Table& t, int32_t K, int32_t L, uint64_t seed, int64_t* idx, int32_t* start, float* w,
                        hipStream_t s);
 hipError_t launch_simple_select(Table& t, int32_t strategy, int32_t B, int32_t L, uint64_t seed,

@@ -92,8 +92,10 @@ __device__ inline void load4_u32(const uint32_t* __restrict__ a, int64_t n, int6
 // of those levels, which this scan zeroes for the next one (each node is
 // zeroed by the chunk that starts it).
 __global__ __launch_bounds__(256) void scan_kernel(const uint32_t* __restrict__ prio, int64_t N, Levels upper,
-                                                   Levels clear, uint64_t* __restrict__ tile_sums, int64_t ntiles) {
+                                                   Levels clear, uint64_t* __restrict__ tile_sums, int64_t ntiles,
+                                                   uint32_t* __restrict__ chunk_min) {
     __shared__ uint64_t tile_sum[kTilesPerChunk];
+    __shared__ uint32_t wave_min[4];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int64_t chunk = blockIdx.x;
@@ -106,6 +108,19 @@ __global__ __launch_bounds__(256) void scan_kernel(const uint32_t* __restrict__ 
     for (int q = 0; q < kTilesPerWave; q++)
         load4_u32(prio, N, (chunk * kTilesPerChunk + wave * kTilesPerWave + q) * kTile + lane * 4, x[q][0], x[q][1],
                   x[q][2], x[q][3]);
+    // Smallest non-zero priority of the chunk (for weights normalised over
+    // the whole table).
+    uint32_t m = 0xFFFFFFFFu;
+#pragma unroll
+    for (int q = 0; q < kTilesPerWave; q++)
+#pragma unroll
+        for (int e = 0; e < 4; e++) m = (x[q][e] != 0u && x[q][e] < m) ? x[q][e] : m;
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+        const uint32_t o = __shfl_xor(m, d);
+        m = o < m ? o : m;
+    }
+    if (lane == 0) wave_min[wave] = m;
 #pragma unroll
     for (int q = 0; q < kTilesPerWave; q++) {
         const uint64_t s = wave_sum((uint64_t)x[q][0] + x[q][1] + x[q][2] + x[q][3]);
@@ -117,6 +132,11 @@ __global__ __launch_bounds__(256) void scan_kernel(const uint32_t* __restrict__ 
     }
     __syncthreads();
     if (wave != 0) return;
+    if (lane == 0) {
+        uint32_t cm = wave_min[0];
+        for (int k = 1; k < 4; k++) cm = wave_min[k] < cm ? wave_min[k] : cm;
+        chunk_min[chunk] = cm;
+    }
     const uint64_t chunk_sum = wave_sum(lane < kTilesPerChunk ? tile_sum[lane] : 0);
     // Lane l - 1 handles level l (>= 1).
     const int l = lane + 1;
@@ -312,7 +332,7 @@ hipError_t launch_scan(Table& t, hipStream_t s) {
     // creation); this scan zeroes the other copy for the next one.
     const int par = 1 - t.tree_parity;
     hipLaunchKernelGGL(scan_kernel, dim3((unsigned)t.nchunks), dim3(256), 0, s, t.priority, t.N, upper_copy(t, par),
-                       upper_copy(t, 1 - par), t.tile_sums, t.ntiles);
+                       upper_copy(t, 1 - par), t.tile_sums, t.ntiles, t.chunk_min);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess) t.tree_parity = par;
     return e;
@@ -335,9 +355,12 @@ hipError_t launch_search(Table& t, int32_t B, int32_t L, uint64_t seed, bool wan
     return hipGetLastError();
 }
 
-hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, float* w, hipStream_t s) {
+hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, float* w, hipStream_t s,
+                             bool global_min) {
+    // The minimum comes from the search's per-workgroup minima of the batch,
+    // or from the scan's per-chunk minima of the whole table.
     hipLaunchKernelGGL(is_weights_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s, B, (double)beta,
-                       t.wg_min, search_grid, w);
+                       global_min ? t.chunk_min : t.wg_min, global_min ? (int)t.nchunks : search_grid, w);
     return hipGetLastError();
 }
 
@@ -400,7 +423,7 @@ extern "C" int gear_select(gear_table* h, int32_t strategy, int32_t B, int32_t L
                                        reinterpret_cast<uint32_t*>(d_weights), &grid, s);
     if (e != hipSuccess) return hip_fail(e, "gear_select: search launch");
     if (weights) {
-        e = gear::launch_is_weights(*t, B, beta, grid, d_weights, s);
+        e = gear::launch_is_weights(*t, B, beta, grid, d_weights, s, (t->options & GEAR_OPT_IS_GLOBAL_MIN) != 0);
         if (e != hipSuccess) return hip_fail(e, "gear_select: weight launch");
     }
     return GEAR_OK;

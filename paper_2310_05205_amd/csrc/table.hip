@@ -62,6 +62,7 @@ void free_table(Table* t) {
     for (int c = 0; c < 2; c++)
         for (int l = 0; l < gear::kMaxLevels; l++) (void)hipFree(t->upper[c][l]);
     (void)hipFree(t->wg_min);
+    (void)hipFree(t->chunk_min);
     (void)hipFree(t->topk_hist);
     (void)hipFree(t->topk_state);
     (void)hipFree(t->topk_local);
@@ -174,6 +175,7 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
             }
         }
     if ((e = dmalloc(&t->wg_min, sizeof(uint32_t) * gear::kSearchMaxGrid)) != hipSuccess) return oom("batch minima", e);
+    if ((e = dmalloc(&t->chunk_min, sizeof(uint32_t) * t->nchunks)) != hipSuccess) return oom("chunk minima", e);
     if ((e = dmalloc(&t->status, sizeof(uint32_t))) != hipSuccess) return oom("status word", e);
     if ((e = dmalloc(&t->topk_hist, sizeof(uint32_t) * 3 * gear::kTopkBins)) != hipSuccess ||
         (e = dmalloc(&t->topk_state, sizeof(uint32_t) * gear::kTopkStateWords)) != hipSuccess ||
@@ -253,8 +255,13 @@ extern "C" int gear_insert(gear_table* h, int64_t n, const void* const* col_src,
 
 extern "C" int gear_table_set_options(gear_table* h, uint32_t options) {
     if (h == nullptr) return fail(GEAR_E_INVAL, "gear_table_set_options: table is NULL");
-    if (options & ~GEAR_OPT_INCREMENTAL_TREE) return fail(GEAR_E_INVAL, "gear_table_set_options: unknown option bits");
-    reinterpret_cast<Table*>(h)->options = options;
+    if (options & ~(GEAR_OPT_INCREMENTAL_TREE | GEAR_OPT_IS_GLOBAL_MIN))
+        return fail(GEAR_E_INVAL, "gear_table_set_options: unknown option bits");
+    Table* t = reinterpret_cast<Table*>(h);
+    // Chunk minima are exact only right after a scan: switching the global
+    // normalisation on forces the next prioritized select to rescan.
+    if ((options & GEAR_OPT_IS_GLOBAL_MIN) && !(t->options & GEAR_OPT_IS_GLOBAL_MIN)) t->cdf_dirty = true;
+    t->options = options;
     return GEAR_OK;
 }
 

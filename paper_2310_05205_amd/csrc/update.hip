@@ -229,7 +229,10 @@ extern "C" int gear_update_priorities(gear_table* h, const int64_t* d_idx, const
     if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_update_priorities: hipSetDevice");
     // Keep the tree current only if it is current now; otherwise the next
     // prioritized select rescans anyway.
-    const bool maintain = (t->options & GEAR_OPT_INCREMENTAL_TREE) && !t->cdf_dirty;
+    // Under global IS normalisation the next select rescans anyway, for the
+    // chunk minima, so the tree is not maintained.
+    const bool maintain = (t->options & GEAR_OPT_INCREMENTAL_TREE) && !(t->options & GEAR_OPT_IS_GLOBAL_MIN) &&
+                          !t->cdf_dirty;
     hipError_t e = gear::launch_scatter(*t, d_idx, d_new_priorities, B, maintain, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "gear_update_priorities: launch");
     if (!maintain) t->cdf_dirty = true;

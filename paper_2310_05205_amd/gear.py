@@ -32,6 +32,7 @@ GEAR_PRIORITIZED = 3
 GEAR_TOPK = 4
 GEAR_MAX_TOPK = 16384
 GEAR_OPT_INCREMENTAL_TREE = 1
+GEAR_OPT_IS_GLOBAL_MIN = 2
 
 
 class GearError(RuntimeError):

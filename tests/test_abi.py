@@ -27,6 +27,13 @@ def test_every_declared_symbol_is_exported():
         assert hasattr(lib, n), n
 
 
+def test_every_exported_symbol_is_declared():
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", gear.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r" T (gear_[a-z_]+)$", out, flags=re.M))
+    assert exported and exported <= set(_declared()), sorted(exported - set(_declared()))
+
+
 def test_header_constants_match_binding():
     with open(os.path.join(ROOT, "include", "gear.h")) as f:
         text = f.read()
