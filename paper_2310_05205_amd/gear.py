@@ -30,6 +30,9 @@ GEAR_LIFO = 1
 GEAR_UNIFORM = 2
 GEAR_PRIORITIZED = 3
 GEAR_TOPK = 4
+GEAR_MAX_CAPACITY = 1 << 30
+GEAR_MAX_COLUMNS = 64
+GEAR_MAX_BATCH = 1 << 24
 GEAR_MAX_TOPK = 16384
 GEAR_OPT_INCREMENTAL_TREE = 1
 GEAR_OPT_IS_GLOBAL_MIN = 2
