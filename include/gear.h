@@ -90,7 +90,9 @@ typedef struct gear_table gear_table;
  *   device      HIP device ordinal that runs the kernels
  *   out         receives the table handle
  *
- * Column c is laid out as [capacity][T][elem_bytes[c]] bytes.  The store
+ * Column c is laid out as [capacity][T][elem_bytes[c]] bytes, all zero
+ * at creation (pinned columns are cleared through their mapped address, at
+ * host-link speed).  The store
  * also owns the uint32 priority array [capacity] (zero = not selectable,
  * Sec. 3.2 index manager) in HBM, and the scan, search and scatter scratch,
  * all sized by `capacity` at creation; no later call allocates except
@@ -125,7 +127,7 @@ int gear_table_destroy(gear_table *t);
 int gear_insert(gear_table *t, int64_t n, const void *const *col_src, const uint32_t *priorities,
                 void *stream);
 /* On a table with an index manager, gear_insert is one gear_allocate of n,
- * the row copies into the allocated blocks, and one gear_commit of the n
+ * gear_write_rows into the allocated slots, and one gear_commit of the n
  * indices with `priorities` (GEAR_E_INSUFFICIENT if pending + n would exceed
  * the maximum). */
 
@@ -188,6 +190,24 @@ int gear_allocate(gear_table *t, int64_t n, int64_t *idx_out, void *stream);
  * nothing changes), GEAR_E_HIP.
  */
 int gear_commit(gear_table *t, int64_t n, const int64_t *idx, const uint32_t *priorities, void *stream);
+
+/*
+ * gear_write_rows - write n trajectories into given slots in place (the
+ * client's write of Sec. 3.2, for data already on a device): row r of every
+ * column source goes to slot idx[r].  Any table; with an index manager the
+ * slots are normally ones just allocated, committed afterwards.
+ *
+ *   idx      host int64[n], slots in [0, capacity)
+ *   col_src  host array of ncols pointers, col_src[c] holding n*T*elem_bytes[c]
+ *            bytes ([n][T][elem_bytes[c]]); device or pinned host memory is
+ *            read by one scatter kernel per column, pageable host memory by
+ *            one copy per run of consecutive slots
+ *
+ * Enqueued on `stream`; sources must stay valid until it completes.  The
+ * rows of a slot listed twice are written in unspecified order.
+ * Errors: GEAR_E_INVAL, GEAR_E_HIP.
+ */
+int gear_write_rows(gear_table *t, int64_t n, const int64_t *idx, const void *const *col_src, void *stream);
 
 /* gear_allocator_info - committed, pending and free index counts of a table
  * with an index manager.  Any output may be NULL.  Errors: GEAR_E_INVAL. */

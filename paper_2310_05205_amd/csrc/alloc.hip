@@ -19,9 +19,14 @@
 // call's decisions are a few integer operations per index.  The device keeps
 // a copy of the commit-order ring (FIFO, LIFO and uniform selection read it)
 // and a committed flag per slot (priority updates of other slots are
-// dropped).  Index lists reach the device through a ring of pinned staging
-// buffers; a buffer is refilled only after the copy out of it has completed,
-// so the host waits only when every buffer still has a copy in flight.
+// dropped).  Index lists reach the device through the table's ring of pinned
+// staging buffers; a buffer is refilled only after the copy out of it has
+// completed, so the host waits only when every buffer still has a copy in
+// flight.
+//
+// Rows are written into their slots by one scatter kernel per column (any
+// slot order), or, from pageable host memory that kernels cannot read, by
+// one copy per run of consecutive slots.
 #include <algorithm>
 #include <cstring>
 #include <new>
@@ -52,6 +57,58 @@ __global__ void commit_kernel(const int64_t* __restrict__ idx, const uint32_t* _
     int64_t pos = pos0 + j;
     if (pos >= N) pos -= N;
     order[pos] = (int32_t)i;
+}
+
+// Row scatter: row r of a contiguous [n][row] source goes to slot idx[r] of
+// a column ([N][row]).  A workgroup copies one piece of up to kRowPiece
+// elements of one row; table-bound loads are non-temporal (the rows are read
+// once), stores are plain.
+constexpr int kRowThreads = 256;
+constexpr int kRowUnroll = 4;
+constexpr int64_t kRowPiece = kRowThreads * kRowUnroll;
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+template <typename V>
+__global__ __launch_bounds__(kRowThreads) void scatter_rows_kernel(const int64_t* __restrict__ idx,
+                                                                   const V* __restrict__ src, V* __restrict__ dst,
+                                                                   int64_t row_elems, int64_t pieces_per_row) {
+    const int64_t q = blockIdx.x;
+    const int64_t r = q / pieces_per_row;
+    const int64_t off = (q - r * pieces_per_row) * kRowPiece;
+    const int64_t len = row_elems - off < kRowPiece ? row_elems - off : kRowPiece;
+    const V* s = src + r * row_elems + off;
+    V* d = dst + idx[r] * row_elems + off;
+    if (len == kRowPiece) {
+        V v[kRowUnroll];
+#pragma unroll
+        for (int k = 0; k < kRowUnroll; k++) v[k] = __builtin_nontemporal_load(s + threadIdx.x + k * kRowThreads);
+#pragma unroll
+        for (int k = 0; k < kRowUnroll; k++) d[threadIdx.x + k * kRowThreads] = v[k];
+    } else {
+        for (int64_t e = threadIdx.x; e < len; e += kRowThreads) d[e] = __builtin_nontemporal_load(s + e);
+    }
+}
+
+template <typename V>
+hipError_t launch_rows(const int64_t* d_idx, int64_t n, const uint8_t* src, uint8_t* dst, int64_t row_bytes,
+                       hipStream_t s) {
+    const int64_t row_elems = row_bytes / (int64_t)sizeof(V);
+    const int64_t ppr = (row_elems + kRowPiece - 1) / kRowPiece;
+    hipLaunchKernelGGL(scatter_rows_kernel<V>, dim3((unsigned)(n * ppr)), dim3(kRowThreads), 0, s, d_idx,
+                       reinterpret_cast<const V*>(src), reinterpret_cast<V*>(dst), row_elems, ppr);
+    return hipGetLastError();
+}
+
+// Whether a kernel on the table's device can read `p` (device memory, or
+// pinned / mapped host memory); pageable host memory cannot.
+bool device_readable(const void* p) {
+    hipPointerAttribute_t a;
+    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+        (void)hipGetLastError();  // clear the error a pageable pointer leaves
+        return false;
+    }
+    return a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeHost || a.type == hipMemoryTypeManaged;
 }
 
 // Copies `count` (<= kStageRows) host indices to t.stage_idx on stream s.
@@ -93,22 +150,50 @@ int64_t release_victim(Table& t) {
 void free_index_manager(Table& t) {
     (void)hipFree(t.order);
     (void)hipFree(t.committed);
-    (void)hipFree(t.stage_idx);
-    (void)hipFree(t.stage_prio);
-    if (t.pin_idx) (void)hipHostFree(t.pin_idx);
-    for (int k = 0; k < kStageSlots; k++) {
-        if (t.pin_free[k]) (void)hipEventDestroy(t.pin_free[k]);
-        t.pin_free[k] = nullptr;
-    }
     t.order = nullptr;
     t.committed = nullptr;
-    t.stage_idx = nullptr;
-    t.stage_prio = nullptr;
-    t.pin_idx = nullptr;
     std::vector<int32_t>().swap(t.free_q);
     std::vector<int32_t>().swap(t.order_h);
     std::vector<uint8_t>().swap(t.slot_state);
     t.managed = false;
+}
+
+int write_rows(Table& t, int64_t n, const int64_t* idx, const void* const* col_src, hipStream_t s) {
+    for (int c = 0; c < t.ncols; c++) {
+        const int64_t rb = (int64_t)t.T * t.elem_bytes[c];
+        uint8_t* base = t.col_dev[c];  // the mapped device address for pinned tables
+        const uint8_t* src = static_cast<const uint8_t*>(col_src[c]);
+        if (!device_readable(src)) {
+            // Pageable host source: one copy per run of consecutive slots.
+            uint8_t* hbase = t.residency == GEAR_HOST_PINNED ? t.col_host[c] : t.col_dev[c];
+            int64_t r0 = 0;
+            while (r0 < n) {
+                int64_t r1 = r0 + 1;
+                while (r1 < n && idx[r1] == idx[r1 - 1] + 1) r1++;
+                hipError_t e = hipMemcpyAsync(hbase + (size_t)idx[r0] * rb, src + (size_t)r0 * rb,
+                                              (size_t)(r1 - r0) * rb, hipMemcpyDefault, s);
+                if (e != hipSuccess) return hip_fail(e, "row copy");
+                r0 = r1;
+            }
+            continue;
+        }
+        const uintptr_t align = reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(base) | (uintptr_t)rb;
+        for (int64_t off = 0; off < n; off += kStageRows) {
+            const int64_t cnt = std::min(n - off, kStageRows);
+            hipError_t e = stage_indices(t, idx + off, cnt, s);
+            if (e == hipSuccess) {
+                const uint8_t* sc = src + (size_t)off * rb;
+                if (align % 16 == 0)
+                    e = launch_rows<u32x4_t>(t.stage_idx, cnt, sc, base, rb, s);
+                else if (align % 4 == 0)
+                    e = launch_rows<uint32_t>(t.stage_idx, cnt, sc, base, rb, s);
+                else
+                    e = launch_rows<uint8_t>(t.stage_idx, cnt, sc, base, rb, s);
+            }
+            if (e != hipSuccess) return hip_fail(e, "row scatter");
+        }
+    }
+    return GEAR_OK;
 }
 
 int managed_insert(Table& t, int64_t n, const void* const* col_src, const uint32_t* priorities, hipStream_t s) {
@@ -123,21 +208,8 @@ int managed_insert(Table& t, int64_t n, const void* const* col_src, const uint32
     gear_table* h = reinterpret_cast<gear_table*>(&t);
     int rc = gear_allocate(h, n, idx.data(), s);
     if (rc != GEAR_OK) return rc;
-    // Write each row into its slot in place, one copy per run of consecutive slots.
-    for (int c = 0; c < t.ncols; c++) {
-        const size_t rb = (size_t)t.T * (size_t)t.elem_bytes[c];
-        uint8_t* base = t.residency == GEAR_HOST_PINNED ? t.col_host[c] : t.col_dev[c];
-        const uint8_t* src = static_cast<const uint8_t*>(col_src[c]);
-        int64_t r0 = 0;
-        while (r0 < n) {
-            int64_t r1 = r0 + 1;
-            while (r1 < n && idx[r1] == idx[r1 - 1] + 1) r1++;
-            hipError_t e = hipMemcpyAsync(base + (size_t)idx[r0] * rb, src + (size_t)r0 * rb,
-                                          (size_t)(r1 - r0) * rb, hipMemcpyDefault, s);
-            if (e != hipSuccess) return hip_fail(e, "gear_insert: row copy");
-            r0 = r1;
-        }
-    }
+    rc = write_rows(t, n, idx.data(), col_src, s);
+    if (rc != GEAR_OK) return rc;
     return gear_commit(h, n, idx.data(), priorities, s);
 }
 
@@ -169,17 +241,11 @@ extern "C" int gear_table_use_allocator(gear_table* h, int32_t removal, int64_t 
     for (int64_t i = 0; i < t->N; i++) t->free_q[(size_t)i] = (int32_t)i;  // every index free, in index order
     hipError_t e;
     if ((e = hipMalloc(reinterpret_cast<void**>(&t->order), sizeof(int32_t) * (size_t)t->N)) != hipSuccess ||
-        (e = hipMalloc(reinterpret_cast<void**>(&t->committed), (size_t)t->N)) != hipSuccess ||
-        (e = hipMalloc(reinterpret_cast<void**>(&t->stage_idx), sizeof(int64_t) * gear::kStageRows)) != hipSuccess ||
-        (e = hipMalloc(reinterpret_cast<void**>(&t->stage_prio), sizeof(uint32_t) * gear::kStageRows)) != hipSuccess ||
-        (e = hipHostMalloc(reinterpret_cast<void**>(&t->pin_idx),
-                           sizeof(int64_t) * gear::kStageRows * gear::kStageSlots, hipHostMallocDefault)) != hipSuccess) {
+        (e = hipMalloc(reinterpret_cast<void**>(&t->committed), (size_t)t->N)) != hipSuccess) {
         gear::free_index_manager(*t);
         return fail(GEAR_E_NOMEM, "gear_table_use_allocator: device arrays");
     }
-    for (int k = 0; k < gear::kStageSlots && e == hipSuccess; k++)
-        e = hipEventCreateWithFlags(&t->pin_free[k], hipEventDisableTiming);
-    if (e != hipSuccess || (e = hipMemset(t->committed, 0, (size_t)t->N)) != hipSuccess ||
+    if ((e = hipMemset(t->committed, 0, (size_t)t->N)) != hipSuccess ||
         (e = hipDeviceSynchronize()) != hipSuccess) {
         gear::free_index_manager(*t);
         return hip_fail(e, "gear_table_use_allocator: initialising");
@@ -270,6 +336,22 @@ extern "C" int gear_commit(gear_table* h, int64_t n, const int64_t* idx, const u
     t->next_seq += (uint64_t)n;
     t->cdf_dirty = true;
     return GEAR_OK;
+}
+
+extern "C" int gear_write_rows(gear_table* h, int64_t n, const int64_t* idx, const void* const* col_src,
+                               void* stream) {
+    if (h == nullptr) return fail(GEAR_E_INVAL, "gear_write_rows: table is NULL");
+    Table* t = reinterpret_cast<Table*>(h);
+    if (n < 0) return fail(GEAR_E_INVAL, "gear_write_rows: n < 0");
+    if (n == 0 || t->ncols == 0) return GEAR_OK;
+    if (idx == nullptr || col_src == nullptr) return fail(GEAR_E_INVAL, "gear_write_rows: NULL pointer argument");
+    for (int c = 0; c < t->ncols; c++)
+        if (col_src[c] == nullptr) return fail(GEAR_E_INVAL, "gear_write_rows: a column source is NULL");
+    for (int64_t r = 0; r < n; r++)
+        if (idx[r] < 0 || idx[r] >= t->N) return fail(GEAR_E_INVAL, "gear_write_rows: a slot is out of range");
+    gear::DeviceGuard guard(t->device);
+    if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_write_rows: hipSetDevice");
+    return gear::write_rows(*t, n, idx, col_src, static_cast<hipStream_t>(stream));
 }
 
 extern "C" int gear_allocator_info(const gear_table* h, int64_t* committed, int64_t* pending, int64_t* free_count) {

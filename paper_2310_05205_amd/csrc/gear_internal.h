@@ -85,6 +85,7 @@ struct Table {
     int64_t ord_head = 0, n_committed = 0, n_pending = 0;
     int32_t* order = nullptr;         // device copy of order_h (same positions)
     uint8_t* committed = nullptr;     // device [N]: 1 for committed slots
+    // Staging of host index and priority lists (every table).
     int64_t* stage_idx = nullptr;     // device staging [kStageRows]
     uint32_t* stage_prio = nullptr;   // device staging [kStageRows]
     int64_t* pin_idx = nullptr;       // pinned host staging [kStageSlots][kStageRows]
@@ -134,6 +135,8 @@ void free_index_manager(Table& t);
 // Managed insertion used by gear_insert: allocate n, copy the rows into the
 // allocated slots, commit them with their priorities.
 int managed_insert(Table& t, int64_t n, const void* const* col_src, const uint32_t* priorities, hipStream_t s);
+// Writes row r of each column source into slot idx[r] (host list) in place.
+int write_rows(Table& t, int64_t n, const int64_t* idx, const void* const* col_src, hipStream_t s);
 // Live count of a table: committed slots (managed) or min(next_seq, N) (ring).
 inline int64_t live_count(const Table& t) {
     if (t.managed) return t.n_committed;

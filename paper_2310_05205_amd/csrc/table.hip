@@ -49,6 +49,11 @@ namespace {
 void free_table(Table* t) {
     if (!t) return;
     gear::free_index_manager(*t);
+    (void)hipFree(t->stage_idx);
+    (void)hipFree(t->stage_prio);
+    if (t->pin_idx) (void)hipHostFree(t->pin_idx);
+    for (int k = 0; k < gear::kStageSlots; k++)
+        if (t->pin_free[k]) (void)hipEventDestroy(t->pin_free[k]);
     for (int c = 0; c < t->ncols; c++) {
         if (t->residency == GEAR_HOST_PINNED) {
             if (t->col_host[c]) (void)hipHostFree(t->col_host[c]);
@@ -130,7 +135,7 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
         if (residency == GEAR_DEVICE) {
             e = hipMalloc(reinterpret_cast<void**>(&t->col_dev[c]), bytes);
             if (e != hipSuccess) return oom("a device column", e);
-            // Slots never inserted read as zeros, as pinned host pages do.
+            // Slots never inserted read as zeros.
             e = hipMemsetAsync(t->col_dev[c], 0, bytes, nullptr);
             if (e != hipSuccess) {
                 free_table(t);
@@ -148,6 +153,13 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
             e = hipHostGetDevicePointer(&d, h, 0);
             if (e != hipSuccess) return oom("a device view of a pinned column", e);
             t->col_dev[c] = static_cast<uint8_t*>(d);
+            // Slots never inserted read as zeros: pinned memory the runtime
+            // hands out again after a free keeps its old contents.
+            e = hipMemsetAsync(t->col_dev[c], 0, bytes, nullptr);
+            if (e != hipSuccess) {
+                free_table(t);
+                return hip_fail(e, "gear_table_create: clearing a pinned column");
+            }
         }
     }
 
@@ -177,6 +189,17 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
     if ((e = dmalloc(&t->wg_min, sizeof(uint32_t) * gear::kSearchMaxGrid)) != hipSuccess) return oom("batch minima", e);
     if ((e = dmalloc(&t->chunk_min, sizeof(uint32_t) * t->nchunks)) != hipSuccess) return oom("chunk minima", e);
     if ((e = dmalloc(&t->status, sizeof(uint32_t))) != hipSuccess) return oom("status word", e);
+    // Staging for host index and priority lists (row writes, index manager).
+    if ((e = dmalloc(&t->stage_idx, sizeof(int64_t) * gear::kStageRows)) != hipSuccess ||
+        (e = dmalloc(&t->stage_prio, sizeof(uint32_t) * gear::kStageRows)) != hipSuccess ||
+        (e = hipHostMalloc(reinterpret_cast<void**>(&t->pin_idx), sizeof(int64_t) * gear::kStageRows * gear::kStageSlots,
+                           hipHostMallocDefault)) != hipSuccess)
+        return oom("index staging", e);
+    for (int k = 0; k < gear::kStageSlots; k++)
+        if ((e = hipEventCreateWithFlags(&t->pin_free[k], hipEventDisableTiming)) != hipSuccess) {
+            free_table(t);
+            return hip_fail(e, "gear_table_create: staging events");
+        }
     if ((e = dmalloc(&t->topk_hist, sizeof(uint32_t) * 3 * gear::kTopkBins)) != hipSuccess ||
         (e = dmalloc(&t->topk_state, sizeof(uint32_t) * gear::kTopkStateWords)) != hipSuccess ||
         (e = dmalloc(&t->topk_local, sizeof(uint32_t) * 3 * gear::kTopkMaxGrid * gear::kTopkBins)) != hipSuccess ||

@@ -72,6 +72,7 @@ def lib():
         L.gear_commit.argtypes = [vp, i64, vp, vp, vp]
         pi64 = ctypes.POINTER(i64)
         L.gear_allocator_info.argtypes = [vp, pi64, pi64, pi64]
+        L.gear_write_rows.argtypes = [vp, i64, vp, vp, vp]
         L.gear_shard_total.argtypes = [vp, vp, vp]
         L.gear_select_shard.argtypes = [vp, i32, i32, vp, i64, i32, i32, u64, vp, vp, vp, vp]
         L.gear_is_weights.argtypes = [vp, vp, i32, ctypes.c_float, vp, vp]
@@ -79,7 +80,7 @@ def lib():
         for name in ["gear_table_create", "gear_table_destroy", "gear_insert", "gear_select", "gear_collect",
                      "gear_update_priorities", "gear_table_sync", "gear_table_info", "gear_table_column",
                      "gear_table_priorities", "gear_table_set_options", "gear_table_use_allocator",
-                     "gear_allocate", "gear_commit", "gear_allocator_info", "gear_shard_total",
+                     "gear_allocate", "gear_commit", "gear_allocator_info", "gear_write_rows", "gear_shard_total",
                      "gear_select_shard", "gear_is_weights", "gear_topk_merge"]:
             getattr(L, name).restype = ctypes.c_int
         L.gear_last_error.argtypes = []
@@ -186,6 +187,13 @@ def gear_commit(table, idx, priorities, stream=0):
     import numpy as np
     idx = np.ascontiguousarray(idx, dtype=np.int64)
     _check(lib().gear_commit(table, idx.size, idx.ctypes.data, priorities, stream))
+
+
+def gear_write_rows(table, idx, col_src, stream=0):
+    """idx: host int64 numpy array; col_src: list of pointers (host or device)."""
+    import numpy as np
+    idx = np.ascontiguousarray(idx, dtype=np.int64)
+    _check(lib().gear_write_rows(table, idx.size, idx.ctypes.data, _ptr_array(col_src), stream))
 
 
 def gear_allocator_info(table):
@@ -319,6 +327,10 @@ class Table:
 
     def allocator_info(self):
         return gear_allocator_info(self.handle)
+
+    def write_rows(self, idx, col_src, stream=None):
+        """Write row r of each column source (tensors/arrays [n, T*E_c]) into slot idx[r]."""
+        gear_write_rows(self.handle, idx, [_data_ptr(x) for x in col_src], self._stream(stream))
 
     def shard_total(self, out, stream=None):
         """Writes this table's priority total into `out` (a one-element int64

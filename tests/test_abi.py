@@ -66,6 +66,7 @@ def test_argument_validation_without_device():
     assert lib.gear_commit(None, 1, None, None, None) == gear.GEAR_E_INVAL
     assert lib.gear_allocator_info(None, None, None, None) == gear.GEAR_E_INVAL
     assert lib.gear_shard_total(None, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_write_rows(None, 1, None, None, None) == gear.GEAR_E_INVAL
     assert lib.gear_select_shard(None, 1, 0, None, 0, 1, 1, 0, None, None, None, None) == gear.GEAR_E_INVAL
     assert lib.gear_is_weights(None, None, 1, ctypes.c_float(0), None, None) == gear.GEAR_E_INVAL
     assert lib.gear_topk_merge(None, None, 0, 1, 1, 1, 0, None, None, None, None, None) == gear.GEAR_E_INVAL

@@ -231,3 +231,97 @@ def test_allocator_errors():
             r.use_allocator(gear.GEAR_FIFO, 8)         # the ring already holds insertions
     finally:
         r.close()
+
+
+ODD_COLS = (gen.Column("b3", gen.BYTES, 3), gen.Column("w12", gen.INT_MOD, 3, param=7),
+            gen.Column("v64", gen.NORMAL_F32, 16))
+
+
+@pytest.mark.parametrize("source", ["device", "pinned", "device-misaligned"])
+@pytest.mark.parametrize("residency", [gear.GEAR_DEVICE, gear.GEAR_HOST_PINNED], ids=["hbm", "pinned"])
+def test_row_scatter_kernel_paths(source, residency):
+    # gear_insert with LIFO removal (victims released newest first, so slots
+    # come in descending order) from device-readable sources: the scatter
+    # kernel with 16-, 4- and 1-byte elements (rows of 48, 36... bytes, and a
+    # source one byte off alignment).
+    N, T, M = 700, 3, 500
+    eb = [c.elem_bytes for c in ODD_COLS]
+    t = gear.Table(eb, N, T, residency, DEV)
+    store = oracle.Store(eb, N, T)
+    try:
+        t.use_allocator(gear.GEAR_LIFO, M)
+        store.use_allocator(oracle.LIFO, M)
+        k = 0
+        for it, n in enumerate([500, 300, 499, 7]):
+            say("row scatter %s residency=%d batch %d" % (source, residency, it))
+            rows = [gen.fill_rows_list_cpu(c, ci, 9, T, np.arange(k, k + n)) for ci, c in enumerate(ODD_COLS)]
+            prio = gen.insert_priorities(U1000, 9, k, n)
+            k += n
+            if source == "pinned":
+                srcs = [torch.from_numpy(r).pin_memory() for r in rows]
+            elif source == "device":
+                srcs = [torch.from_numpy(r).to(cuda()) for r in rows]
+            else:
+                bufs = [torch.zeros(r.size + 1, dtype=torch.uint8, device=cuda()) for r in rows]
+                for b_, r in zip(bufs, rows):
+                    b_[1:] = torch.from_numpy(r.reshape(-1)).to(cuda())
+                srcs = [b_[1:] for b_ in bufs]
+            t.insert(srcs, prio)
+            assert store.insert(rows, prio) == oracle.OK
+            torch.cuda.synchronize(DEV)
+            for c in range(len(ODD_COLS)):
+                view = t.column_view(c)
+                got = view if isinstance(view, np.ndarray) else host(view)
+                np.testing.assert_array_equal(got, store.cols[c], err_msg="column %d" % c)
+            _check_state(t, store, "batch %d" % it)
+    finally:
+        t.close()
+
+
+U1000 = gen.PrioDist(gen.PRIO_UNIFORM, 1, 1000)
+
+
+def test_write_rows_on_a_ring_table():
+    # Writes into arbitrary slots of a ring table, any order, then collect.
+    N, T = 300, 4
+    eb = [c.elem_bytes for c in COLS]
+    t = gear.Table(eb, N, T, gear.GEAR_DEVICE, DEV)
+    store = oracle.Store(eb, N, T)
+    try:
+        prio = np.arange(1, N + 1, dtype=np.uint32)
+        rows0 = _rows(np.arange(N), T)
+        t.insert([np.ascontiguousarray(r) for r in rows0], prio)
+        store.insert(rows0, prio)
+        rng = np.random.default_rng(5)
+        slots = rng.permutation(N)[:120].astype(np.int64)
+        rows = _rows(np.arange(1000, 1120), T)
+        t.write_rows(slots, [torch.from_numpy(np.ascontiguousarray(r)).to(cuda()) for r in rows])
+        store.write(slots, rows)
+        idx = torch.from_numpy(rng.integers(0, N, size=256).astype(np.int64)).to(cuda())
+        start = torch.zeros(256, dtype=torch.int32, device=cuda())
+        outs = t.collect(idx, start, T)
+        st, oouts = store.collect(host(idx), host(start), T)
+        for a, b in zip(outs, oouts):
+            np.testing.assert_array_equal(host(a), b)
+        with pytest.raises(gear.GearError):
+            t.write_rows(np.array([N], np.int64), [torch.zeros(T * e, dtype=torch.uint8, device=cuda()) for e in eb])
+        assert t.sync() == 0
+    finally:
+        t.close()
+
+
+def test_new_tables_read_zero_after_reuse():
+    # Freed pinned (and device) memory can come back with old contents; a new
+    # table must still read as zeros in every slot never written.
+    for residency in (gear.GEAR_HOST_PINNED, gear.GEAR_DEVICE):
+        for _ in range(3):
+            t = gear.Table([40], 2000, 5, residency, DEV)
+            v = t.column_view(0)
+            if isinstance(v, np.ndarray):
+                assert not v.any()
+                v[:] = 0xFF
+            else:
+                assert int(v.count_nonzero()) == 0
+                v.fill_(0xFF)
+            torch.cuda.synchronize(DEV)
+            t.close()
