@@ -212,11 +212,15 @@ def cpu_baseline(w, target_s, global_min=False):
 
 def run_insert(args):
     """Insertion through the index manager on the MAT-shaped HBM table, full
-    and in steady state (every new trajectory releases the oldest, FIFO).
-    One step: allocate B indices (victims' priorities zeroed on the device),
-    write B new trajectories in place through the column views (the client's
-    scatter, here torch indexing from device-resident rows), commit B with
-    device-side priorities.  Prints one JSON line with its own metric."""
+    and in steady state (every new trajectory releases a victim), once with
+    FIFO and once with LIFO removal.  Per step and removal:
+      write_rows  allocate B indices, write B device-resident trajectories into
+                  them with gear_write_rows (one scatter kernel per column),
+                  commit B with device-side priorities;
+      insert      the same through one gear_insert call;
+    and, FIFO only, the client's own scatter through the column views (torch
+    indexing) in place of gear_write_rows.  Prints one JSON line with its own
+    metric: trajectories inserted per second by the write_rows path, FIFO."""
     import numpy as np
     import torch
 
@@ -230,99 +234,103 @@ def run_insert(args):
     w = configs.MAT
     dev = torch.device("cuda", 0)
     sh = torch.cuda.current_stream(dev).cuda_stream
-    t = gear.Table(w.elem_bytes, w.N, w.T, gear.GEAR_DEVICE, 0)
-    t.use_allocator(gear.GEAR_FIFO, w.N)
-    fill_table(w, lambda n, ptrs, prio: t.insert(ptrs, prio), device=0)
     B, K, W = w.B, args.steps, args.warmup
+    row_bytes = w.T * sum(w.elem_bytes)
     # B new trajectories, generated in HBM: insertions N .. N+B-1 of the workload.
     rows = [torch.empty((B, w.T * c.elem_bytes), dtype=torch.uint8, device=dev) for c in w.columns]
     for ci, c in enumerate(w.columns):
         gen.fill_rows_gpu(c, ci, w.seed, w.T, w.n_insert, B, rows[ci].data_ptr(), sh)
+    ptrs = [r.data_ptr() for r in rows]
     prio = torch.from_numpy(gen.insert_priorities(w.prio, w.seed, w.n_insert, B)).to(dev)
-    views = [t.column_view(c) for c in range(len(w.columns))]
     hev = HipEvents()
 
-    def step(ev=None):
-        h0 = time.perf_counter()
-        if ev:
-            hev.record(ev[0], sh)
-        idx = t.allocate(B)
-        if ev:
-            hev.record(ev[1], sh)
-        h1 = time.perf_counter()
-        d_idx = torch.from_numpy(idx).to(dev)
-        for c, r in enumerate(rows):
-            views[c][d_idx] = r
-        if ev:
-            hev.record(ev[2], sh)
-        h2 = time.perf_counter()
-        t.commit(idx, prio)
-        if ev:
-            hev.record(ev[3], sh)
-        h3 = time.perf_counter()
-        return h1 - h0, h3 - h2
+    def timed(fn, stages=1):
+        for _ in range(W):
+            fn(None)
+        torch.cuda.synchronize()
+        evs = [[hev.create() for _ in range(stages + 1)] for _ in range(K)]
+        t0 = time.perf_counter()
+        for k in range(K):
+            fn(evs[k])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ms = [float(np.mean([hev.elapsed_ms(e[j], e[j + 1]) for e in evs])) for j in range(stages)]
+        return wall, ms
 
-    for _ in range(W):
-        step()
-    torch.cuda.synchronize()
-    evs = [[hev.create() for _ in range(4)] for _ in range(K)]
-    host_alloc, host_commit = [], []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(K):
-        a, c = step(evs[k])
-        host_alloc.append(a)
-        host_commit.append(c)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    if t.sync() != 0:
-        raise SystemExit("device status set during the insert steps")
-    committed, pending, free = t.allocator_info()
-    assert committed == w.N and pending == 0
-    alloc_ms = float(np.mean([hev.elapsed_ms(e[0], e[1]) for e in evs]))
-    write_ms = float(np.mean([hev.elapsed_ms(e[1], e[2]) for e in evs]))
-    commit_ms = float(np.mean([hev.elapsed_ms(e[2], e[3]) for e in evs]))
+    results = {}
+    for removal, name in ((gear.GEAR_FIFO, "fifo"), (gear.GEAR_LIFO, "lifo")):
+        t = gear.Table(w.elem_bytes, w.N, w.T, gear.GEAR_DEVICE, 0)
+        t.use_allocator(removal, w.N)
+        fill_table(w, lambda n, p_, q_: t.insert(p_, q_), device=0)
+        views = [t.column_view(c) for c in range(len(w.columns))]
 
-    # The library's own insertion: gear_insert = allocate, row copies into the
-    # allocated blocks (one per run of consecutive slots), commit.
-    ptrs = [r.data_ptr() for r in rows]
-    for _ in range(W):
-        t.insert(ptrs, prio)
-    torch.cuda.synchronize()
-    iev = [(hev.create(), hev.create()) for _ in range(K)]
-    t1 = time.perf_counter()
-    for k in range(K):
-        hev.record(iev[k][0], sh)
-        t.insert(ptrs, prio)
-        hev.record(iev[k][1], sh)
-    torch.cuda.synchronize()
-    wall_insert = time.perf_counter() - t1
-    ins_ms = float(np.mean([hev.elapsed_ms(a, b) for a, b in iev]))
-    if t.sync() != 0:
-        raise SystemExit("device status set during the gear_insert steps")
+        def write_rows_step(ev):
+            if ev:
+                hev.record(ev[0], sh)
+            idx = t.allocate(B)
+            if ev:
+                hev.record(ev[1], sh)
+            gear.gear_write_rows(t.handle, idx, ptrs, sh)
+            if ev:
+                hev.record(ev[2], sh)
+            t.commit(idx, prio)
+            if ev:
+                hev.record(ev[3], sh)
+
+        def insert_step(ev):
+            if ev:
+                hev.record(ev[0], sh)
+            t.insert(ptrs, prio)
+            if ev:
+                hev.record(ev[1], sh)
+
+        def client_step(ev):
+            if ev:
+                hev.record(ev[0], sh)
+            idx = t.allocate(B)
+            d_idx = torch.from_numpy(idx).to(dev)
+            for c, r in enumerate(rows):
+                views[c][d_idx] = r
+            if ev:
+                hev.record(ev[1], sh)
+            t.commit(idx, prio)
+
+        wall_w, (a_ms, w_ms, c_ms) = timed(write_rows_step, 3)
+        wall_i, (i_ms,) = timed(insert_step, 1)
+        r = {"write_rows_path": {"trajectories_per_s": round(B * K / wall_w, 1), "ms_per_step": round(wall_w * 1e3 / K, 5),
+                                 "allocate_ms": round(a_ms, 5), "write_ms": round(w_ms, 5), "commit_ms": round(c_ms, 5),
+                                 "write_GBps": round(2 * B * row_bytes / (w_ms * 1e-3) / 1e9, 1)},
+             "gear_insert": {"trajectories_per_s": round(B * K / wall_i, 1), "ms_per_call": round(i_ms, 5),
+                             "GBps": round(2 * B * row_bytes / (i_ms * 1e-3) / 1e9, 1)}}
+        if removal == gear.GEAR_FIFO:
+            wall_c, (s_ms,) = timed(client_step, 1)
+            r["client_torch_scatter"] = {"trajectories_per_s": round(B * K / wall_c, 1),
+                                         "allocate_and_scatter_ms": round(s_ms, 5)}
+        committed, pending, free = t.allocator_info()
+        assert committed == w.N and pending == 0
+        if t.sync() != 0:
+            raise SystemExit("device status set during the insert steps")
+        del views
+        t.close()
+        results[name] = r
     hev.close()
-    row_bytes = w.T * sum(w.elem_bytes)
+    fifo = results["fifo"]["write_rows_path"]
     line = {
         "metric": "trajectories inserted/sec through allocate + in-place write + commit",
-        "value": round(B * K / wall, 1), "unit": "trajectories/s", "n_gpus": 1, "steps": K, "warmup": W,
-        "ms_per_step": round(wall * 1e3 / K, 5), "higher_is_better": True, "scaling": "weak",
+        "value": fifo["trajectories_per_s"], "unit": "trajectories/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": fifo["ms_per_step"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "u8", "data": "synthetic",
-        "config": {"workload": "mat-insert N=500000 T=200 B=8192 (FIFO removal, table full)", "N": w.N,
+        "config": {"workload": "mat-insert N=500000 T=200 B=8192 (table full, FIFO then LIFO removal)", "N": w.N,
                    "T": w.T, "B": B, "elem_bytes": w.elem_bytes, "table_bytes": w.table_bytes,
                    "parallelism": "1 GPU"},
-        "trajectory_steps_per_s": round(B * w.T * K / wall, 1),
-        "stages_ms": {"allocate": round(alloc_ms, 5), "write": round(write_ms, 5), "commit": round(commit_ms, 5),
-                      "note": "HIP events around each stage in the timed steps; write is the client's scatter"},
-        "host_ms": {"allocate": round(1e3 * float(np.mean(host_alloc)), 4),
-                    "commit": round(1e3 * float(np.mean(host_commit)), 4)},
-        "write_GBps": round(2 * B * row_bytes / (write_ms * 1e-3) / 1e9, 1),
-        "gear_insert": {"trajectories_per_s": round(B * K / wall_insert, 1), "ms_per_call": round(ins_ms, 5),
-                        "copy_GBps": round(2 * B * row_bytes / (ins_ms * 1e-3) / 1e9, 1),
-                        "note": "gear_insert of the same B device-resident rows: allocate, one copy per run of "
-                                "consecutive slots per column, commit"},
-        "roofline": None, "cpu_baseline": None,
+        "by_removal": results,
+        "roofline": {"bound": "hbm", "achieved": fifo["write_GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(fifo["write_GBps"] / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "scatter_rows_kernel", "algorithmic_bytes_per_launch": 2 * B * row_bytes,
+                     "note": "bytes of the three per-column launches of one gear_write_rows call, "
+                             "over the events around that call"},
+        "cpu_baseline": None,
     }
-    t.close()
     print(json.dumps(line), flush=True)
 
 
