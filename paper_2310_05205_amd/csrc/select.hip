@@ -91,6 +91,9 @@ __device__ inline void load4_u32(const uint32_t* __restrict__ a, int64_t n, int6
 // `upper` holds the levels >= 1 this scan adds into; `clear` the other copy
 // of those levels, which this scan zeroes for the next one (each node is
 // zeroed by the chunk that starts it).
+// kMin: also write the chunk's smallest non-zero priority (only the
+// global IS normalisation needs it; the plain scan stays minimal).
+template <bool kMin>
 __global__ __launch_bounds__(256) void scan_kernel(const uint32_t* __restrict__ prio, int64_t N, Levels upper,
                                                    Levels clear, uint64_t* __restrict__ tile_sums, int64_t ntiles,
                                                    uint32_t* __restrict__ chunk_min) {
@@ -108,19 +111,6 @@ __global__ __launch_bounds__(256) void scan_kernel(const uint32_t* __restrict__ 
     for (int q = 0; q < kTilesPerWave; q++)
         load4_u32(prio, N, (chunk * kTilesPerChunk + wave * kTilesPerWave + q) * kTile + lane * 4, x[q][0], x[q][1],
                   x[q][2], x[q][3]);
-    // Smallest non-zero priority of the chunk (for weights normalised over
-    // the whole table).
-    uint32_t m = 0xFFFFFFFFu;
-#pragma unroll
-    for (int q = 0; q < kTilesPerWave; q++)
-#pragma unroll
-        for (int e = 0; e < 4; e++) m = (x[q][e] != 0u && x[q][e] < m) ? x[q][e] : m;
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) {
-        const uint32_t o = __shfl_xor(m, d);
-        m = o < m ? o : m;
-    }
-    if (lane == 0) wave_min[wave] = m;
 #pragma unroll
     for (int q = 0; q < kTilesPerWave; q++) {
         const uint64_t s = wave_sum((uint64_t)x[q][0] + x[q][1] + x[q][2] + x[q][3]);
@@ -130,9 +120,23 @@ __global__ __launch_bounds__(256) void scan_kernel(const uint32_t* __restrict__ 
             if (gt < ntiles) tile_sums[gt] = s;
         }
     }
+    if (kMin) {
+        // Smallest non-zero priority of the chunk.
+        uint32_t m = 0xFFFFFFFFu;
+#pragma unroll
+        for (int q = 0; q < kTilesPerWave; q++)
+#pragma unroll
+            for (int e = 0; e < 4; e++) m = (x[q][e] != 0u && x[q][e] < m) ? x[q][e] : m;
+#pragma unroll
+        for (int d = 32; d >= 1; d >>= 1) {
+            const uint32_t o = __shfl_xor(m, d);
+            m = o < m ? o : m;
+        }
+        if (lane == 0) wave_min[wave] = m;
+    }
     __syncthreads();
     if (wave != 0) return;
-    if (lane == 0) {
+    if (kMin && lane == 0) {
         uint32_t cm = wave_min[0];
         for (int k = 1; k < 4; k++) cm = wave_min[k] < cm ? wave_min[k] : cm;
         chunk_min[chunk] = cm;
@@ -158,6 +162,7 @@ struct Shard {
     int64_t base;            // added to the local slot of an owned draw
 };
 
+template <bool kShard>
 __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict__ prio, int64_t N, Levels lv,
                                                      int32_t B, uint64_t span, uint64_t seed, int want_min,
                                                      Shard sh, uint32_t* __restrict__ wg_min, uint32_t* status,
@@ -176,7 +181,7 @@ __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict_
     const uint64_t S = read_lane(tc3, 63);
     // Draws are numbers in [0, S_all); this table owns [P, P + S).
     uint64_t S_all = S, P = 0;
-    if (sh.totals) {
+    if (kShard) {
         uint64_t all = 0, before = 0;
         for (int h = lane; h < sh.G; h += 64) {
             const uint64_t x = sh.totals[h];
@@ -199,7 +204,7 @@ __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict_
             continue;
         }
         uint64_t r = scale_draw(splitmix64_out(seed, 2 * (uint64_t)b), S_all);
-        if (sh.totals) {
+        if (kShard) {
             if (r < P || r - P >= S) {  // another shard's draw: same window start, no slot
                 if (lane == 0) {
                     idx[b] = -1;
@@ -224,7 +229,7 @@ __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict_
         wave_prefix4(p0, p1, p2, p3, c0, c1, c2, c3);
         const int cnt = pick_child(c0, c1, c2, c3, r);
         if (lane == 0) {
-            idx[b] = sh.base + j * kTile + cnt;
+            idx[b] = (kShard ? sh.base : 0) + j * kTile + cnt;
             start[b] = (int32_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b + 1), span);
         }
         if (want_min) {
@@ -331,8 +336,12 @@ hipError_t launch_scan(Table& t, hipStream_t s) {
     // The copy this scan fills was zeroed by the previous scan (or at
     // creation); this scan zeroes the other copy for the next one.
     const int par = 1 - t.tree_parity;
-    hipLaunchKernelGGL(scan_kernel, dim3((unsigned)t.nchunks), dim3(256), 0, s, t.priority, t.N, upper_copy(t, par),
-                       upper_copy(t, 1 - par), t.tile_sums, t.ntiles, t.chunk_min);
+    if (t.options & GEAR_OPT_IS_GLOBAL_MIN)
+        hipLaunchKernelGGL(scan_kernel<true>, dim3((unsigned)t.nchunks), dim3(256), 0, s, t.priority, t.N,
+                           upper_copy(t, par), upper_copy(t, 1 - par), t.tile_sums, t.ntiles, t.chunk_min);
+    else
+        hipLaunchKernelGGL(scan_kernel<false>, dim3((unsigned)t.nchunks), dim3(256), 0, s, t.priority, t.N,
+                           upper_copy(t, par), upper_copy(t, 1 - par), t.tile_sums, t.ntiles, t.chunk_min);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess) t.tree_parity = par;
     return e;
@@ -348,9 +357,14 @@ hipError_t launch_search(Table& t, int32_t B, int32_t L, uint64_t seed, bool wan
     sh.G = G;
     sh.g = g;
     sh.base = base;
-    hipLaunchKernelGGL(search_kernel, dim3(grid), dim3(256), 0, s, t.priority, t.N, tree(t), B,
-                       (uint64_t)(t.T - L + 1), seed, want_min ? 1 : 0, sh, t.wg_min, t.status, idx, start,
-                       sel_prio);
+    if (shard_totals)
+        hipLaunchKernelGGL(search_kernel<true>, dim3(grid), dim3(256), 0, s, t.priority, t.N, tree(t), B,
+                           (uint64_t)(t.T - L + 1), seed, want_min ? 1 : 0, sh, t.wg_min, t.status, idx, start,
+                           sel_prio);
+    else
+        hipLaunchKernelGGL(search_kernel<false>, dim3(grid), dim3(256), 0, s, t.priority, t.N, tree(t), B,
+                           (uint64_t)(t.T - L + 1), seed, want_min ? 1 : 0, sh, t.wg_min, t.status, idx, start,
+                           sel_prio);
     *grid_out = grid;
     return hipGetLastError();
 }
