@@ -15,8 +15,7 @@
 // TopK (decentralized): every shard computes its local top-K, sorted; one
 // GPU merges the G sorted lists (gear_topk_merge).  A candidate's place in
 // the merged order is its place in its own list plus, for every other
-// list, the number of entries that come before it there (a binary search):
-// O(G*K*G*log K) work, no sort.
+// list, the number of entries that come before it there: no sort.
 #include "gear_internal.h"
 #include "wave.h"
 
@@ -72,34 +71,211 @@ __global__ void merge_fill_kernel(int32_t K, int64_t* __restrict__ idx, int32_t*
     if (out_prio) out_prio[k] = 0u;
 }
 
-// Thread t: entry j = t mod K of list g = t / K.  Lists are sorted in
-// candidate order with their -1 entries last.
-__global__ void merge_kernel(const uint32_t* __restrict__ prio, const int64_t* __restrict__ gidx, int32_t G,
-                             int32_t K, uint64_t span, uint64_t seed, int64_t* __restrict__ idx,
-                             int32_t* __restrict__ start, float* __restrict__ w, uint32_t* __restrict__ out_prio) {
-    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= (int64_t)G * K) return;
-    const int g = (int)(t / K);
-    const int64_t i = gidx[t];
-    if (i < 0) return;
-    const uint32_t p = prio[t];
-    int64_t place = t - (int64_t)g * K;
-    for (int h = 0; h < G && place < K; h++) {
-        if (h == g) continue;
-        const uint32_t* ph = prio + (int64_t)h * K;
-        const int64_t* ih = gidx + (int64_t)h * K;
-        int lo = 0, hi = K;  // first entry of list h that does not come before (p, i)
-        while (lo < hi) {
-            const int mid = (lo + hi) >> 1;
-            const int64_t im = ih[mid];
-            if (im >= 0 && before(ph[mid], im, p, i))
-                lo = mid + 1;
-            else
-                hi = mid;
+// Merge of G sorted lists by ranks.  A workgroup takes a tile of
+// kMergeTile consecutive entries of list g, kMergeParts threads per entry.
+// The entries of another list h that come before a tile entry are all of h
+// up to a point that moves forward along the tile, so for the whole tile
+// they lie between two positions of h: the ranks in h of the tile's first
+// and last valid entries.  Those two ranks, for every other list of a round
+// of kMergeRound lists, are found by cooperative searches of kProbeLanes
+// lanes each; the entries between them (the bracket) go to LDS; and each
+// thread finishes the ranks of its entry in its share of the round's lists
+// by binary searches in LDS.  A bracket that does not fit in LDS is
+// searched in global memory instead.  Binary searches by every thread
+// straight over global memory cost about eight times more load
+// instructions; one thread per entry leaves one wave per SIMD.
+constexpr int kMergeThreads = 256;
+constexpr int kMergeParts = 4;                          // threads per tile entry
+constexpr int kMergeTile = kMergeThreads / kMergeParts;  // 64 entries
+constexpr int kMergeRound = 8;                           // lists per round: 2 * 8 searches, 4 per wave
+constexpr int kListsPerPart = kMergeRound / kMergeParts;
+constexpr int kProbeLanes = 16;                          // lanes per cooperative search
+constexpr int kBracketCap = 1024;                        // bracket entries in LDS per round (12 KiB)
+constexpr int kFillPerThread = kBracketCap / kMergeThreads;
+
+// Entries of list (ph, ih) of length K that come before (p, i), by the 16
+// lanes of group `grp` of the wave (lane `sub` within it).  Valid entries
+// form a sorted prefix, so "comes before" is true on a prefix of positions.
+// Each round probes 15 evenly spaced positions of the remaining range and
+// keeps the piece between the last probe that comes before and the first
+// that does not; a range of at most 16 positions is probed whole.  Every
+// lane of the wave must call this (the rounds use wave ballots).
+__device__ int group_count_before(const uint32_t* __restrict__ ph, const int64_t* __restrict__ ih, int K, uint32_t p,
+                                  int64_t i, bool active, int grp, int sub) {
+    int lo = 0, hi = K;  // the count lies in [lo, hi]
+    bool done = !active;
+    int count = 0;
+    while (__ballot(!done) != 0) {
+        const int n = hi - lo;
+        const bool whole = n <= kProbeLanes;
+        const int q = whole ? lo + sub : lo + ((sub + 1) * n) / kProbeLanes - 1;
+        bool pred = false;
+        if (!done && sub < (whole ? n : kProbeLanes - 1)) {
+            const int64_t iq = ih[q];  // both loads issued before either is used
+            const uint32_t pq = ph[q];
+            pred = (iq >= 0) & before(pq, iq, p, i);
         }
-        place += lo;
+        const int c = __popcll((__ballot(pred) >> (grp * kProbeLanes)) & 0xFFFFull);
+        if (!done) {
+            if (whole) {
+                count = lo + c;
+                done = true;
+            } else {
+                const int nlo = c > 0 ? lo + (c * n) / kProbeLanes : lo;
+                const int nhi = c < kProbeLanes - 1 ? lo + ((c + 1) * n) / kProbeLanes - 1 : hi;
+                lo = nlo;
+                hi = nhi;
+            }
+        }
     }
-    if (place >= K) return;
+    return count;
+}
+
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(const uint32_t* __restrict__ prio,
+                                                              const int64_t* __restrict__ gidx, int32_t G, int32_t K,
+                                                              uint64_t span, uint64_t seed, int64_t* __restrict__ idx,
+                                                              int32_t* __restrict__ start, float* __restrict__ w,
+                                                              uint32_t* __restrict__ out_prio) {
+    __shared__ uint32_t s_p[kBracketCap];
+    __shared__ int64_t s_i[kBracketCap];
+    __shared__ int s_lo[kMergeRound], s_hi[kMergeRound], s_off[kMergeRound];
+    __shared__ int s_steps;
+    __shared__ uint32_t s_kp[2];
+    __shared__ int64_t s_ki[2];
+    const int tiles = (K + kMergeTile - 1) / kMergeTile;
+    const int g = (int)(blockIdx.x / tiles);
+    const int entry = (int)threadIdx.x / kMergeParts, part = (int)threadIdx.x % kMergeParts;
+    const int j = (int)(blockIdx.x % tiles) * kMergeTile + entry;
+    const int64_t at = (int64_t)g * K + j;
+    const int64_t i = j < K ? gidx[at] : -1;
+    const uint32_t p = j < K ? prio[at] : 0u;
+    // Valid entries are a prefix of the list, hence of the tile.
+    const int nvalid = __syncthreads_count(i >= 0 && part == 0);
+    if (nvalid == 0) return;
+    if (threadIdx.x == 0) {
+        s_kp[0] = p;
+        s_ki[0] = i;
+    }
+    if ((int)threadIdx.x == (nvalid - 1) * kMergeParts) {
+        s_kp[1] = p;
+        s_ki[1] = i;
+    }
+    __syncthreads();
+    const int wave = (int)threadIdx.x >> 6, lane = (int)threadIdx.x & 63;
+    const int grp = lane / kProbeLanes, sub = lane % kProbeLanes;
+    const int search = wave * (64 / kProbeLanes) + grp;  // 0 .. 2 * kMergeRound - 1
+    const int su = search >> 1, end = search & 1;         // list in the round; 0: first entry, 1: last entry
+    int count = 0;
+    for (int h0 = 0; h0 < G; h0 += kMergeRound) {
+        {
+            const int h = h0 + su;
+            const bool act = h < G && h != g;
+            const int r = group_count_before(prio + (int64_t)(act ? h : 0) * K, gidx + (int64_t)(act ? h : 0) * K, K,
+                                             s_kp[end], s_ki[end], act, grp, sub);
+            if (act && sub == 0) (end ? s_hi : s_lo)[su] = r;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int used = 0, widest = 0;
+            for (int u = 0; u < kMergeRound; u++) {
+                const int h = h0 + u;
+                if (h >= G || h == g) {
+                    s_lo[u] = s_hi[u] = 0;
+                    s_off[u] = 0;
+                    continue;
+                }
+                const int wdt = s_hi[u] - s_lo[u];
+                widest = wdt > widest ? wdt : widest;
+                if (used + wdt <= kBracketCap) {
+                    s_off[u] = used;
+                    used += wdt;
+                } else {
+                    s_off[u] = -1;
+                }
+            }
+            s_steps = 32 - __clz((unsigned)widest);  // halvings that empty the widest bracket
+        }
+        __syncthreads();
+        int r_off[kMergeRound], r_lo[kMergeRound], r_w[kMergeRound];
+#pragma unroll
+        for (int u = 0; u < kMergeRound; u++) {
+            r_off[u] = s_off[u];
+            r_lo[u] = s_lo[u];
+            r_w[u] = s_hi[u] - s_lo[u];
+        }
+        {
+            // Every bracket entry of the round, kFillPerThread per thread at
+            // most: all loads are issued before the first LDS store.
+            uint32_t vp[kFillPerThread];
+            int64_t vi[kFillPerThread];
+            int dst[kFillPerThread];
+#pragma unroll
+            for (int k = 0; k < kFillPerThread; k++) {
+                const int e = (int)threadIdx.x + k * kMergeThreads;
+                dst[k] = -1;
+                int64_t a = 0;
+#pragma unroll
+                for (int u = 0; u < kMergeRound; u++) {
+                    if (r_off[u] >= 0 && e >= r_off[u] && e < r_off[u] + r_w[u]) {
+                        a = (int64_t)(h0 + u) * K + r_lo[u] + (e - r_off[u]);
+                        dst[k] = e;
+                    }
+                }
+                if (dst[k] >= 0) {
+                    vp[k] = prio[a];
+                    vi[k] = gidx[a];
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < kFillPerThread; k++) {
+                if (dst[k] >= 0) {
+                    s_p[dst[k]] = vp[k];
+                    s_i[dst[k]] = vi[k];
+                }
+            }
+        }
+        __syncthreads();
+        if (i >= 0) {
+            // This thread's lists of the round: part, part + kMergeParts, ...
+            int lo[kListsPerPart], hi[kListsPerPart];
+#pragma unroll
+            for (int v = 0; v < kListsPerPart; v++) {
+                lo[v] = 0;
+                hi[v] = r_w[part + v * kMergeParts];
+            }
+            const int steps = s_steps;
+            for (int step = 0; step < steps; step++) {
+#pragma unroll
+                for (int v = 0; v < kListsPerPart; v++) {
+                    if (lo[v] < hi[v]) {
+                        const int u = part + v * kMergeParts;
+                        const int mid = (lo[v] + hi[v]) >> 1;
+                        uint32_t pm;
+                        int64_t im;
+                        if (r_off[u] >= 0) {
+                            pm = s_p[r_off[u] + mid];
+                            im = s_i[r_off[u] + mid];
+                        } else {
+                            const int64_t a = (int64_t)(h0 + u) * K + r_lo[u] + mid;
+                            pm = prio[a];
+                            im = gidx[a];
+                        }
+                        if (before(pm, im, p, i))
+                            lo[v] = mid + 1;
+                        else
+                            hi[v] = mid;
+                    }
+                }
+            }
+#pragma unroll
+            for (int v = 0; v < kListsPerPart; v++) count += r_lo[part + v * kMergeParts] + lo[v];
+        }
+        __syncthreads();  // the next round overwrites the brackets
+    }
+    // The parts of one entry are adjacent lanes of one wave.
+    for (int off = kMergeParts >> 1; off > 0; off >>= 1) count += __shfl_xor(count, off);
+    const int64_t place = (int64_t)j + count;
+    if (i < 0 || part != 0 || place >= K) return;
     idx[place] = i;
     start[place] = (int32_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)place + 1), span);
     if (w) w[place] = 1.0f;
@@ -193,7 +369,8 @@ extern "C" int gear_topk_merge(const uint32_t* d_prio, const int64_t* d_gidx, in
                        d_weights, d_out_prio);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess) {
-        hipLaunchKernelGGL(gear::merge_kernel, dim3(gear::blocks_for((int64_t)G * K)), dim3(256), 0, s, d_prio, d_gidx,
+        const int64_t tiles = ((int64_t)K + gear::kMergeTile - 1) / gear::kMergeTile;
+        hipLaunchKernelGGL(gear::merge_kernel, dim3((unsigned)(G * tiles)), dim3(gear::kMergeThreads), 0, s, d_prio, d_gidx,
                            G, K, (uint64_t)(T - L + 1), seed, d_idx, d_start, d_weights, d_out_prio);
         e = hipGetLastError();
     }

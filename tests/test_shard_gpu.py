@@ -90,11 +90,18 @@ def test_all_shards_empty_sets_no_weight():
             t.close()
 
 
+U3 = gen.PrioDist(gen.PRIO_UNIFORM, 1, 3)
+# G2-wide-brackets: 64 neighbouring entries of the sparse shard span about
+# 2000 entries of the dense one, more than the merge stages in LDS, so those
+# ranks are searched in global memory.  G12: more than 8 lists, several
+# rounds of brackets.
 TOPK_CASES = [(1, 5000, [PARETO], 777), (4, 20000, [PARETO], 8192), (8, 3000, [U, None], 5000),
-              (3, 100, [U], 1000), (6, 50000, [gen.PrioDist(gen.PRIO_UNIFORM, 1, 3)], 16384)]
+              (3, 100, [U], 1000), (6, 50000, [U3], 16384), (2, 3000, [U, U3], 5000),
+              (12, 2000, [U, PARETO, U3], 3000)]
 
 
-@pytest.mark.parametrize("G,cap,dists,K", TOPK_CASES, ids=["G1", "G4-pareto", "G8-zero-shards", "G3-short", "G6-ties"])
+@pytest.mark.parametrize("G,cap,dists,K", TOPK_CASES,
+                         ids=["G1", "G4-pareto", "G8-zero-shards", "G3-short", "G6-ties", "G2-wide-brackets", "G12"])
 def test_topk_merge_equals_concatenated(G, cap, dists, K):
     T, L = 5, 2
     tabs, P = _shards(G, cap, dists, T=T)
