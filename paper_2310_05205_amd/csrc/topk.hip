@@ -17,8 +17,8 @@
 //
 //   topk_hist_kernel    (x3) a workgroup histograms one digit of the keys
 //                       whose higher digits match the ones chosen so far,
-//                       in LDS (lanes of a wave that share a bin are peeled
-//                       off with one atomic for the whole group), adds its
+//                       in LDS (the lanes of a wave that share the first
+//                       lane's bin add with one atomic), adds its
 //                       bins into the pass's global histogram and stores the
 //                       suffix sums of its own histogram.
 //   topk_compact_kernel derives the threshold; the stored suffix sums give
@@ -215,15 +215,17 @@ __global__ __launch_bounds__(kTopkThreads) void topk_hist_kernel(const uint32_t*
                 const uint64_t key = order_key(p);
                 bool left = p != 0u && (pass == 0 || (key >> prev_shift) == prev.prefix);
                 const uint32_t bin = (uint32_t)(key >> shift) & (uint32_t)(kBins - 1);
-                uint64_t vm = __ballot(left);
-                for (int r = 0; r < 3 && vm != 0; r++) {
+                // The lanes that share the first counted lane's bin (most
+                // lanes, when the priorities are skewed) add once; the rest
+                // add one each.  A second or third such round measured
+                // slower than the atomics it saves.
+                const uint64_t vm = __ballot(left);
+                if (vm != 0) {
                     const int first = __ffsll((long long)vm) - 1;
                     const uint32_t b0 = (uint32_t)__builtin_amdgcn_readlane((int)bin, first);
                     const uint64_t m = __ballot(left && bin == b0);
                     if (lane == first) atomicAdd(&sh[b0], (uint32_t)__popcll(m));
                     left = left && bin != b0;
-                    vm &= ~m;
-                    if (__popcll(m) < 4) break;
                 }
                 if (left) atomicAdd(&sh[bin], 1u);
             }
