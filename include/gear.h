@@ -12,9 +12,13 @@
  *                HBM or in pinned host memory read zero-copy by the kernel.
  *
  * Conventions for every call:
- *   - Return value: GEAR_OK (0) or a negative GEAR_E_* code.  A failing call
- *     enqueues nothing and leaves the table unchanged; gear_last_error()
- *     then returns a message for the calling thread.
+ *   - Return value: GEAR_OK (0) or a negative GEAR_E_* code, with a message
+ *     for the calling thread in gear_last_error().  A call that returns
+ *     GEAR_E_INVAL, GEAR_E_EMPTY or GEAR_E_INSUFFICIENT has enqueued nothing
+ *     and left the table unchanged.  After GEAR_E_HIP or GEAR_E_NOMEM from a
+ *     call that enqueues work, part of that work may have been enqueued or
+ *     recorded (an insertion may have written some columns, an allocation
+ *     released some victims); the table should then be closed.
  *   - `stream` is a hipStream_t passed as void*; NULL means the null stream.
  *     Every device-side effect is enqueued on `stream` and is asynchronous
  *     to the host; only gear_table_sync() blocks.
