@@ -597,8 +597,13 @@ def main():
             gear.gear_update_priorities(t.handle, idx.data_ptr(), newp[it].data_ptr(), B, sh)
         hev.record(e[3], sh)
     torch.cuda.synchronize()
-    sel_ms = float(np.mean([hev.elapsed_ms(e[0], e[1]) for e in sev]))
-    upd_ms = float(np.mean([hev.elapsed_ms(e[2], e[3]) for e in sev]))
+    sel_all = [hev.elapsed_ms(e[0], e[1]) for e in sev]
+    col_all = [hev.elapsed_ms(e[1], e[2]) for e in sev]
+    upd_all = [hev.elapsed_ms(e[2], e[3]) for e in sev]
+    sel_ms = float(np.mean(sel_all))
+    upd_ms = float(np.mean(upd_all))
+    pct = {name: [round(float(x), 5) for x in np.percentile(v, [10, 50, 90])]
+           for name, v in (("select", sel_all), ("collect", col_all), ("update", upd_all))}
     hev.close()
 
     if host_table:
@@ -644,6 +649,7 @@ def main():
         "cpu_baseline": cpu,
         "stages_ms": {"select": round(sel_ms, 5), "collect": round(col_ms, 5), "update": round(upd_ms, 5),
                       "note": "select/update from a separate loop after the timed region"},
+        "stages_ms_p10_p50_p90": pct,
         "selection_samples_per_s": round(B / (sel_ms * 1e-3), 1),
         "batch_bytes": batch_bytes,
     }

@@ -28,6 +28,12 @@
  *   - A table is not thread-safe.  All calls on one table must be ordered:
  *     issue them from one host thread, on one stream, or order the streams
  *     with events.  Separate tables are independent.
+ *   - HIP graph capture: gear_collect keeps no host-side state and may be
+ *     captured and replayed.  Selection, insertion, allocation, commits and
+ *     updates read and change host-side state when they are called (ring
+ *     counters, whether the sum tree is current, which copy of its upper
+ *     levels is live), so a replayed capture would repeat stale decisions:
+ *     call them directly.
  *   - Conditions only the device can see (all priorities zero, an index or
  *     window start out of range) are recorded in the table's device status
  *     word, returned and cleared by gear_table_sync().
