@@ -26,7 +26,7 @@ constexpr int kSearchMaxGrid = 2048;
 // TopK: at most this many workgroups per digit pass.
 constexpr int kTopkMaxGrid = 256;
 constexpr int kTopkBins = 4096;       // bins of one TopK digit pass (12-bit digits)
-constexpr int kTopkStateWords = 8;
+constexpr int kTopkStateWords = 32;   // TopK selection states after 0 .. 3 digit passes
 constexpr int kTopkRankBlock = 512;    // keys one TopK rank workgroup compares against
 constexpr int kTopkMaxK = GEAR_MAX_TOPK;
 // Index manager: index lists move to the device in chunks of this many,
@@ -69,7 +69,7 @@ struct Table {
 
     // TopK scratch (fixed sizes).
     uint32_t* topk_hist = nullptr;    // [3][kTopkBins] digit histograms, zero between calls
-    uint32_t* topk_state = nullptr;   // [kTopkStateWords] selection state after the digit passes
+    uint32_t* topk_state = nullptr;   // [kTopkStateWords] selection states after 0 .. 3 digit passes
     uint32_t* topk_local = nullptr;   // [3][kTopkMaxGrid][kTopkBins] per-workgroup suffix sums of each digit pass
     // Index manager (allocate / commit insertion), off for ring tables.  The
     // host keeps the free-index queue, every slot's state and the committed

@@ -11,9 +11,10 @@
 // bins (every value below 256 is one bin) and spread skewed distributions
 // over many bins.  Selection stops early once the chosen bin is a single
 // value or is taken whole.  No workgroup waits for another and no kernel
-// fences memory: each kernel re-derives the digits chosen so far from the
-// complete histograms of the earlier passes, made visible by the kernel
-// boundary.
+// fences memory: workgroup 0 of each kernel stores the selection state it
+// derived, and the next kernel (after the kernel boundary that makes it and
+// the previous pass's complete histogram visible) derives at most one more
+// digit from that histogram.
 //
 //   topk_hist_kernel    (x3) a workgroup histograms one digit of the keys
 //                       whose higher digits match the ones chosen so far,
@@ -21,7 +22,7 @@
 //                       lane's bin add with one atomic), adds its
 //                       bins into the pass's global histogram and stores the
 //                       suffix sums of its own histogram.
-//   topk_compact_kernel derives the threshold; the stored suffix sums give
+//   topk_compact_kernel finishes the threshold; the stored suffix sums give
 //                       every workgroup's count above and at it, hence this
 //                       workgroup's output offsets; one scan per batch of
 //                       loads orders its keys by slot.  It writes
@@ -61,7 +62,7 @@ struct TopkState {
     int32_t passes;   // digits chosen; keys are compared after >> (36 - 12 * passes)
     uint32_t flags;
 };
-static_assert(sizeof(TopkState) <= kTopkStateWords * sizeof(uint32_t), "state buffer");
+static_assert(sizeof(TopkState) * (kPasses + 1) <= kTopkStateWords * sizeof(uint32_t), "state buffer");
 
 // Order-preserving 36-bit key of a non-zero priority (0 maps to 0 like 1;
 // validity is tested separately).
@@ -107,14 +108,9 @@ __device__ __forceinline__ void load_batch(const uint32_t* __restrict__ prio, in
 // thread order is descending bin order; .w is the highest).
 __device__ __forceinline__ int first_bin() { return kBins - 4 - 4 * (int)threadIdx.x; }
 
-struct HistRows {
-    uint4 h[kPasses];
-};
-
-__device__ __forceinline__ void load_rows(const uint32_t* __restrict__ hist, int passes, HistRows& r) {
-#pragma unroll
-    for (int q = 0; q < kPasses; q++)
-        r.h[q] = q < passes ? *reinterpret_cast<const uint4*>(hist + q * kBins + first_bin()) : make_uint4(0, 0, 0, 0);
+// This thread's four bins of digit pass q's global histogram.
+__device__ __forceinline__ uint4 load_row(const uint32_t* __restrict__ hist, int q) {
+    return *reinterpret_cast<const uint4*>(hist + q * kBins + first_bin());
 }
 
 struct DeriveShared {
@@ -168,33 +164,41 @@ __device__ TopkState derive_pass(uint4 h, int q, const TopkState& prev, uint32_t
     return sh.state[q];
 }
 
-// State after at most `passes` digit passes of this call (fewer when an
-// earlier pass already decided).
-__device__ TopkState derive_rows(const HistRows& r, int passes, uint32_t K, DeriveShared& sh) {
+__device__ __forceinline__ TopkState initial_state(uint32_t K) {
     TopkState st;
     st.prefix = 0;
     st.k_rem = K;
     st.total = 0;
     st.passes = 0;
     st.flags = 0;
-#pragma unroll
-    for (int q = 0; q < kPasses; q++) {
-        if (q >= passes || decided(st)) break;
-        st = derive_pass(r.h[q], q, st, K, sh);
-    }
     return st;
+}
+
+// The state after digit passes 0 .. q-1 (q >= 1): the state after passes
+// 0 .. q-2 that the previous kernel stored in states[q - 1] (the initial
+// state when q = 1), advanced by pass q - 1 unless it was already decided.
+// `row` is this thread's part of pass q - 1's histogram, loaded together with
+// the stored state.  Every thread of the block must call this.
+__device__ TopkState state_after(int q, const TopkState& stored, uint4 row, uint32_t K, DeriveShared& sh) {
+    const TopkState s = q >= 2 ? stored : initial_state(K);
+    return decided(s) ? s : derive_pass(row, q - 1, s, K, sh);
 }
 
 __global__ __launch_bounds__(kTopkThreads) void topk_hist_kernel(const uint32_t* __restrict__ prio, int64_t N,
                                                                  int64_t chunk, int pass, uint32_t K,
                                                                  uint32_t* __restrict__ hist,
-                                                                 uint32_t* __restrict__ local) {
+                                                                 uint32_t* __restrict__ local,
+                                                                 TopkState* __restrict__ states) {
     __shared__ __align__(16) uint32_t sh[kBins];
     __shared__ DeriveShared dsh;
     __shared__ uint64_t s_wt[kTopkWaves];
-    HistRows rows;
-    load_rows(hist, pass, rows);
-    const TopkState prev = derive_rows(rows, pass, K, dsh);
+    TopkState prev = initial_state(K);
+    if (pass > 0) {
+        const uint4 row = load_row(hist, pass - 1);
+        const TopkState stored = states[pass - 1];
+        prev = state_after(pass, stored, row, K, dsh);
+        if (blockIdx.x == 0 && threadIdx.x == 0) states[pass] = prev;  // for the next kernel
+    }
     if (decided(prev)) return;  // nothing left to histogram
     const int prev_shift = kKeyBits - kDigit * pass;
     const int shift = prev_shift - kDigit;
@@ -293,21 +297,21 @@ __global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(const uint32
                                                                     int64_t chunk, uint32_t K,
                                                                     const uint32_t* __restrict__ hist,
                                                                     const uint32_t* __restrict__ local, int grid,
-                                                                    TopkState* state,
+                                                                    TopkState* __restrict__ states,
                                                                     uint64_t* __restrict__ keys,
                                                                     uint32_t* __restrict__ rank) {
     __shared__ DeriveShared dsh;
     __shared__ uint64_t s_pre[kVec * kTopkWaves];  // per (load, wave): packed counts, then their prefix
     __shared__ uint64_t s_base[5];                 // above base, at base, total above, own above, own at
     __shared__ uint64_t s_batch;                   // packed counts of the whole batch
-    HistRows rows;
-    load_rows(hist, kPasses, rows);
+    const uint4 row = load_row(hist, kPasses - 1);
+    const TopkState stored = states[kPasses - 1];
     int64_t lo, hi;
     wg_range(N, chunk, lo, hi);
     uint32_t v[kVec][4];
     load_batch(prio, lo, hi, v);
-    const TopkState st = derive_rows(rows, kPasses, K, dsh);
-    if (blockIdx.x == 0 && threadIdx.x == 0) *state = st;
+    const TopkState st = state_after(kPasses, stored, row, K, dsh);
+    if (blockIdx.x == 0 && threadIdx.x == 0) states[kPasses] = st;  // the final state, for rank and emit
     // The rank kernel accumulates into rank: start it at zero.
     for (int k = blockIdx.x * kTopkThreads + threadIdx.x; k < (int)K; k += grid * kTopkThreads) rank[k] = 0u;
     const int shift = state_shift(st);
@@ -476,15 +480,18 @@ hipError_t launch_topk(Table& t, int32_t K, int32_t L, uint64_t seed, int64_t* i
     g = g < kTopkMaxGrid ? g : kTopkMaxGrid;
     const int64_t chunk = ((t.N + g - 1) / g + unit - 1) / unit * unit;
     const int grid = (int)((t.N + chunk - 1) / chunk);
-    TopkState* state = reinterpret_cast<TopkState*>(t.topk_state);
+    // states[q]: the state after digit passes 0 .. q-1, stored by kernel q
+    // (digit pass q, or the compaction for q = kPasses) for the kernels after it.
+    TopkState* states = reinterpret_cast<TopkState*>(t.topk_state);
+    TopkState* state = states + kPasses;
     hipError_t e;
     for (int pass = 0; pass < kPasses; pass++) {
         hipLaunchKernelGGL(topk_hist_kernel, dim3(grid), dim3(kTopkThreads), 0, s, t.priority, t.N, chunk, pass,
-                           (uint32_t)K, t.topk_hist, t.topk_local);
+                           (uint32_t)K, t.topk_hist, t.topk_local, states);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     hipLaunchKernelGGL(topk_compact_kernel, dim3(grid), dim3(kTopkThreads), 0, s, t.priority, t.N, chunk,
-                       (uint32_t)K, t.topk_hist, t.topk_local, grid, state, t.topk_keys, t.topk_rank);
+                       (uint32_t)K, t.topk_hist, t.topk_local, grid, states, t.topk_keys, t.topk_rank);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(topk_rank_kernel, dim3((K + kRankKeys - 1) / kRankKeys, (K + kRankBlock - 1) / kRankBlock),
                        dim3(kRankKeys), 0, s,
