@@ -58,7 +58,9 @@ extern "C" {
 /* Bits of the device status word (gear_table_sync). */
 #define GEAR_STATUS_NO_WEIGHT  1u  /* prioritized select saw a priority total of 0 */
 #define GEAR_STATUS_BAD_INDEX  2u  /* collect/update saw an index or start out of range */
-#define GEAR_STATUS_INTERNAL   4u  /* a kernel's bounded wait expired (library defect) */
+#define GEAR_STATUS_INTERNAL   4u  /* a TopK selection found its own counts inconsistent (priorities
+                                       changed while it ran, against the ordering rule, or a
+                                       library defect); its output is incomplete */
 
 /* Where the column tables live. */
 #define GEAR_DEVICE       0  /* HBM of the table's GPU */
@@ -357,8 +359,8 @@ int gear_topk_merge(const uint32_t *d_prio, const int64_t *d_gidx, int32_t G, in
 
 /*
  * gear_update_priorities - write new priorities for selected slots (Sec. 3.2:
- * the status table holds the priorities; updates are consolidated and
- * committed).  Applied as if in batch order: when a slot appears more than
+ * the status table holds the priorities; changes to it are gathered, then
+ * applied).  Applied as if in batch order: when a slot appears more than
  * once, the last occurrence's value wins.
  *
  *   d_idx            device int64[B], slots in [0, live count) (a table

@@ -343,9 +343,9 @@ int oracle_collect(int32_t ncols, const uint8_t *const *col_base, const int64_t 
 }
 
 /* ------------------------------------------------------------------------ */
-/* Priority update (Sec. 3.2: status-table priorities, updates consolidated  */
-/* and committed).  Applied in batch order, so the last write to a slot      */
-/* wins.  Indices must lie in [0, N).                                        */
+/* Priority update (Sec. 3.2: the status table holds the priorities;       */
+/* changes are gathered, then applied).  Applied in batch order, so the     */
+/* last write to a slot wins.  Indices must lie in [0, N).                  */
 /* ------------------------------------------------------------------------ */
 int oracle_update(uint32_t *priority, int64_t N, const int64_t *idx, const uint32_t *newp, int32_t B)
 {

@@ -1,5 +1,5 @@
 // Priority update on gfx950 (GEAR Sec. 3.2: the status table holds the
-// priorities; updates are consolidated and committed).
+// priorities, and changes to it are gathered and then applied).
 //
 // The batch is applied as if in order, so for a slot that appears several
 // times the last occurrence's value wins.
