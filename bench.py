@@ -259,24 +259,38 @@ def cpu_baseline(w, target_s, global_min=False):
     rows = [gen.fill_rows_list_cpu(c, ci, w.seed, w.T, ks) for ci, c in enumerate(w.columns)]
     local = np.arange(w.B, dtype=np.int64)
     newp = gen.update_priorities(w.prio, w.seed, 0, w.B)
-    reps = 0
-    t0 = time.perf_counter()
-    while True:
-        st, oidx, ostart, ow = oracle.select(strat, p, next_seq, w.T, w.B, w.L, seed, w.beta, True,
-                                             global_min=global_min)
-        if rows:
-            st2, outs = oracle.collect(rows, w.T, local, ostart, w.L)
-            del outs
-        oracle.update(p, oidx, newp)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= target_s:
-            break
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), model)
+    except OSError:
+        pass
+    # The timed loop runs on one core of those this thread may use.
+    allowed = sorted(os.sched_getaffinity(0))
+    core = allowed[-1]
+    os.sched_setaffinity(0, {core})
+    try:
+        reps = 0
+        t0 = time.perf_counter()
+        while True:
+            st, oidx, ostart, ow = oracle.select(strat, p, next_seq, w.T, w.B, w.L, seed, w.beta, True,
+                                                 global_min=global_min)
+            if rows:
+                st2, outs = oracle.collect(rows, w.T, local, ostart, w.L)
+                del outs
+            oracle.update(p, oidx, newp)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= target_s:
+                break
+    finally:
+        os.sched_setaffinity(0, set(allowed))
     return {"value": w.B * w.L * reps / el, "unit": "trajectory-steps/s", "cores": 1, "kind": "oracle",
             "sample": "%d repetitions of one step (%s select over all %d priorities, collect of "
                       "the %d selected %d-step windows from a compact host table of the selected "
                       "trajectories, update) in %.1f s on one host core"
-                      % (reps, {3: "prioritized", 4: "TopK"}.get(strat, "select"), w.N, w.B, w.L, el)}
+                      % (reps, {3: "prioritized", 4: "TopK"}.get(strat, "select"), w.N, w.B, w.L, el),
+            "pinned_core": core, "nproc": os.cpu_count(), "host_cpu": model}
 
 
 def run_insert(args):
