@@ -13,7 +13,7 @@ against its bandwidth peak from HIP events around each gather launch in the
 timed region; `cpu_baseline` is the plain CPU oracle timed on a bounded
 sample of the same workload.
 
-  python bench.py [--steps K] [--warmup W] [--workload mat|gato-host|dt|tiny|select-stress|topk]
+  python bench.py [--steps K] [--warmup W] [--workload mat|gato-host|dt|dt-full|tiny|select-stress|topk|...]
   python bench.py --workload mat-insert   # insertion through the index manager (own metric)
   python bench.py --workload shard-select # one GPU's share of selection over 8 shards (own metric)
   python bench.py --calibrate     # plain copy kernel of known size, for counter scaling
@@ -83,7 +83,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="mat",
-                    choices=["mat", "gato-host", "dt", "tiny", "select-stress", "topk", "mat-insert", "shard-select"])
+                    choices=["mat", "gato-host", "dt", "dt-full", "tiny", "select-stress", "topk", "mat-insert",
+                             "shard-select"])
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
     ap.add_argument("--incremental", action="store_true",
                     help="keep the selection sum tree current across updates (no rescan per step)")
@@ -97,7 +98,8 @@ def parse():
 
 def workload(name):
     from gen import configs
-    return {"mat": configs.MAT, "gato-host": configs.GATO_HOST, "dt": configs.DT, "tiny": configs.TINY,
+    return {"mat": configs.MAT, "gato-host": configs.GATO_HOST, "dt": configs.DT, "dt-full": configs.DT_FULL,
+            "tiny": configs.TINY,
             "select-stress": configs.SELECT_STRESS, "topk": configs.TOPK_STRESS}[name]
 
 
@@ -253,6 +255,7 @@ def cpu_baseline(w, target_s, global_min=False):
     p, next_seq = oracle_priorities(w)
     seed = gen.select_seed(w.seed, 0)
     strat = w.strategies[0]
+    updates = strat in (oracle.PRIORITIZED, oracle.TOPK)  # as in the GPU step
     st, idx, start, _ = oracle.select(strat, p, next_seq, w.T, w.B, w.L, seed, w.beta, True, global_min=global_min)
     assert st == oracle.OK
     ks = gen.slot_insertion(idx, next_seq, w.N)
@@ -278,7 +281,8 @@ def cpu_baseline(w, target_s, global_min=False):
             if rows:
                 st2, outs = oracle.collect(rows, w.T, local, ostart, w.L)
                 del outs
-            oracle.update(p, oidx, newp)
+            if updates:
+                oracle.update(p, oidx, newp)
             reps += 1
             el = time.perf_counter() - t0
             if el >= target_s:
@@ -286,10 +290,11 @@ def cpu_baseline(w, target_s, global_min=False):
     finally:
         os.sched_setaffinity(0, set(allowed))
     return {"value": w.B * w.L * reps / el, "unit": "trajectory-steps/s", "cores": 1, "kind": "oracle",
-            "sample": "%d repetitions of one step (%s select over all %d priorities, collect of "
+            "sample": "%d repetitions of one step (%s select over all %d slots, collect of "
                       "the %d selected %d-step windows from a compact host table of the selected "
-                      "trajectories, update) in %.1f s on one host core"
-                      % (reps, {3: "prioritized", 4: "TopK"}.get(strat, "select"), w.N, w.B, w.L, el),
+                      "trajectories%s) in %.1f s on one host core"
+                      % (reps, {0: "FIFO", 1: "LIFO", 2: "uniform", 3: "prioritized", 4: "TopK"}[strat], w.N, w.B,
+                         w.L, ", update" if updates else "", el),
             "pinned_core": core, "nproc": os.cpu_count(), "host_cpu": model}
 
 
@@ -617,7 +622,8 @@ def main():
     sel_ms = float(np.mean(sel_all))
     upd_ms = float(np.mean(upd_all))
     pct = {name: [round(float(x), 5) for x in np.percentile(v, [10, 50, 90])]
-           for name, v in (("select", sel_all), ("collect", col_all), ("update", upd_all))}
+           for name, v in (("select", sel_all), ("collect", col_all), ("update", upd_all))
+           if name != "update" or prioritized}
     hev.close()
 
     if host_table:
@@ -661,7 +667,8 @@ def main():
                    "is_normalisation": "table minimum" if args.global_min else "batch minimum"},
         "roofline": roof,
         "cpu_baseline": cpu,
-        "stages_ms": {"select": round(sel_ms, 5), "collect": round(col_ms, 5), "update": round(upd_ms, 5),
+        "stages_ms": {"select": round(sel_ms, 5), "collect": round(col_ms, 5),
+                      "update": round(upd_ms, 5) if prioritized else None,
                       "note": "select/update from a separate loop after the timed region"},
         "stages_ms_p10_p50_p90": pct,
         "selection_samples_per_s": round(B / (sel_ms * 1e-3), 1),

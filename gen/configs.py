@@ -68,6 +68,12 @@ DT = Workload(
     n_insert=65536 + 65536 // 8, prio=PrioDist(PRIO_UNIFORM, 1, 1000),
     strategies=(UNIFORM, FIFO, LIFO), B=512, L=20)
 
+# The same table, whole trajectories (L = T): 51.2 MB gathered per batch.
+DT_FULL = Workload(
+    name="dt-full-trajectories N=65536 T=1000 B=512 L=1000",
+    seed=2, N=65536, T=1000, columns=DT.columns, n_insert=DT.n_insert, prio=DT.prio,
+    strategies=(UNIFORM, FIFO, LIFO), B=512, L=1000)
+
 # Selection-only stress: 2^22 Pareto(1.5) priorities, 100 iterations.
 SELECT_STRESS = Workload(
     name="selection-stress N=4194304 B=8192 x100",
@@ -102,4 +108,4 @@ TOPK_STRESS = Workload(
     n_insert=1 << 22, prio=PrioDist(PRIO_PARETO, 1.5, float(1 << 24)),
     strategies=(TOPK,), B=8192, L=1, weights=False, iterations=100)
 
-ALL = (TINY, DT, SELECT_STRESS, GATO_HOST, MAT, TOPK_STRESS)
+ALL = (TINY, DT, DT_FULL, SELECT_STRESS, GATO_HOST, MAT, TOPK_STRESS)

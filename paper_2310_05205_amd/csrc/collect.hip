@@ -14,6 +14,8 @@
 //
 // Element width per column: 16 bytes when every window source and output
 // address is 16-byte aligned, else 4 bytes when 4-byte aligned, else 1.
+// Sources are aligned when the column base and the step size are, or, for
+// full-trajectory windows (L = T, every start 0), the trajectory size.
 #include "gear_internal.h"
 
 namespace gear {
@@ -225,8 +227,11 @@ extern "C" int gear_collect(gear_table* h, const int64_t* d_idx, const int32_t* 
             ct.E = t->elem_bytes[c];
             ct.W = (int64_t)L * ct.E;
             const uintptr_t sa = reinterpret_cast<uintptr_t>(ct.src), oa = reinterpret_cast<uintptr_t>(ct.out);
-            if (ct.E % 16 == 0 && sa % 16 == 0 && oa % 16 == 0) ct.width = 16;
-            else if (ct.E % 4 == 0 && sa % 4 == 0 && oa % 4 == 0) ct.width = 4;
+            // Window sources lie E bytes apart, or T*E when L = T (every
+            // window then starts at step 0); outputs lie W bytes apart.
+            const int64_t stride = L == t->T ? (int64_t)t->T * ct.E : ct.E;
+            if (stride % 16 == 0 && ct.W % 16 == 0 && sa % 16 == 0 && oa % 16 == 0) ct.width = 16;
+            else if (stride % 4 == 0 && ct.W % 4 == 0 && sa % 4 == 0 && oa % 4 == 0) ct.width = 4;
             else ct.width = 1;
             ct.piece = (int64_t)gear::kThreads * gear::kUnroll * ct.width;
             ct.task0 = tasks;

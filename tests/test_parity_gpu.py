@@ -146,6 +146,31 @@ def test_dt_uniform_fifo_lifo_wrapped_ring():
         t.close()
 
 
+def test_dt_full_trajectories():
+    # The bench's full-trajectory workload: 512 whole trajectories (L = T =
+    # 1000) by each strategy, every window against the oracle.
+    w = configs.DT_FULL
+    t = gpu_table(w)
+    try:
+        _, next_seq = t.info()
+        zeros = np.zeros(w.N, dtype=np.uint32)
+        for strat in w.strategies:
+            say("dt-full strategy %d" % strat)
+            seed = gen.select_seed(w.seed, 7)
+            idx, start, _ = t.select(strat, w.B, w.L, seed)
+            st, oidx, ostart, _ = oracle.select(strat, zeros, next_seq, w.T, w.B, w.L, seed)
+            assert st == oracle.OK
+            np.testing.assert_array_equal(host(idx), oidx)
+            assert not np.any(host(start))
+            outs = t.collect(idx, start, w.L)
+            ref = oracle_windows(w, oidx, ostart, w.L, next_seq, np.arange(w.B))
+            for c in range(len(w.columns)):
+                np.testing.assert_array_equal(host(outs[c]), ref[c])
+        assert t.sync() == 0
+    finally:
+        t.close()
+
+
 # ---------------------------------------------------------------------------
 # Edge cases: ragged tails, tiny and multi-level prefix trees, odd element
 # sizes, partial fills, wrap-around, zero runs and large priorities.
@@ -177,6 +202,9 @@ EDGE = [
     _custom("big-batch", 300000, 1, [], 300000, U1000, 12000, 1),
     _custom("wide-narrow-mix", 2000, 40, ODD, 2000, U1000, 700, 33),
     _custom("batch-one", 777, 6, ODD[:3], 777, U1000, 1, 6),
+    # L = T with step sizes of 12 and 68 bytes: every window starts at step
+    # 0, 48 and 272 bytes apart, so the 16-byte path applies.
+    _custom("full-window-16B", 3000, 4, ODD[2:4], 3000, U1000, 500, 4),
 ]
 
 
