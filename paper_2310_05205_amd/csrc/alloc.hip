@@ -19,10 +19,10 @@
 // call's decisions are a few integer operations per index.  The device keeps
 // a copy of the commit-order ring (FIFO, LIFO and uniform selection read it)
 // and a committed flag per slot (priority updates of other slots are
-// dropped).  Index lists reach the device through the table's ring of pinned
-// staging buffers; a buffer is refilled only after the copy out of it has
-// completed, so the host waits only when every buffer still has a copy in
-// flight.
+// dropped).  Index lists reach the device through the table's ring of
+// pinned, mapped staging slots, which the kernels read in place; a slot is
+// refilled only after its last reader has run, so the host waits only when
+// every slot is still in use.
 //
 // Rows are written into their slots by one scatter kernel per column (any
 // slot order), or, from pageable host memory that kernels cannot read, by
@@ -148,36 +148,59 @@ bool device_readable(const void* p) {
     return a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeHost || a.type == hipMemoryTypeManaged;
 }
 
-// Copies `count` (<= kStageRows) host indices to t.stage_idx on stream s.
-// The device buffer is reused in stream order: this copy runs after the
-// kernels that read the previous chunk.
-hipError_t stage_indices(Table& t, const int64_t* host, int64_t count, hipStream_t s) {
-    const int slot = t.pin_next;
-    t.pin_next = (slot + 1) % kStageSlots;
-    int64_t* pin = t.pin_idx + (size_t)slot * kStageRows;
-    hipError_t e = hipEventSynchronize(t.pin_free[slot]);  // the last copy out of this buffer is done
+// One slot of the table's pinned staging ring: a host list is copied into
+// it by the CPU and read in place by the kernels of one chunk.  A slot is
+// refilled only after the event recorded behind its last reader, so the
+// host waits only when every slot is still being read.
+struct PinSlot {
+    int k;
+    int64_t* h_idx;
+    uint32_t* h_prio;
+    const int64_t* d_idx;    // device addresses of the same memory
+    const uint32_t* d_prio;
+};
+
+hipError_t acquire_slot(Table& t, PinSlot& ps) {
+    ps.k = t.pin_next;
+    t.pin_next = (ps.k + 1) % kStageSlots;
+    const hipError_t e = hipEventSynchronize(t.pin_free[ps.k]);
     if (e != hipSuccess) return e;
-    std::memcpy(pin, host, sizeof(int64_t) * (size_t)count);
-    e = hipMemcpyAsync(t.stage_idx, pin, sizeof(int64_t) * (size_t)count, hipMemcpyHostToDevice, s);
-    if (e != hipSuccess) return e;
-    return hipEventRecord(t.pin_free[slot], s);
+    const int64_t off = (int64_t)ps.k * kStageSlotBytes;
+    const int64_t prio_off = off + kStageRows * (int64_t)sizeof(int64_t);
+    ps.h_idx = reinterpret_cast<int64_t*>(t.pin_host + off);
+    ps.h_prio = reinterpret_cast<uint32_t*>(t.pin_host + prio_off);
+    ps.d_idx = reinterpret_cast<const int64_t*>(t.pin_dev + off);
+    ps.d_prio = reinterpret_cast<const uint32_t*>(t.pin_dev + prio_off);
+    return hipSuccess;
+}
+
+// Call after enqueuing the last kernel that reads the slot.
+hipError_t release_slot(Table& t, const PinSlot& ps, hipStream_t s) { return hipEventRecord(t.pin_free[ps.k], s); }
+
+__global__ void copy_list_kernel(const int64_t* __restrict__ src, int64_t n, int64_t* __restrict__ dst) {
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j < n) dst[j] = src[j];
 }
 
 unsigned blocks_for(int64_t n) { return (unsigned)((n + 255) / 256); }
 
 // Releases one victim by the removal strategy (host state only).
+// Positions in the rings are below N and counts at most N, so a sum of the
+// two wraps with one subtraction (no division in these per-index loops).
+inline int64_t wrap(int64_t pos, int64_t N) { return pos >= N ? pos - N : pos; }
+
 int64_t release_victim(Table& t) {
     int64_t pos;
     if (t.removal == GEAR_FIFO) {
         pos = t.ord_head;
-        t.ord_head = t.ord_head + 1 == t.N ? 0 : t.ord_head + 1;
+        t.ord_head = wrap(t.ord_head + 1, t.N);
     } else {
-        pos = (t.ord_head + t.n_committed - 1) % t.N;
+        pos = wrap(t.ord_head + t.n_committed - 1, t.N);
     }
-    const int32_t v = t.order_h[pos];
+    const int32_t v = t.order_h[(size_t)pos];
     t.n_committed--;
-    t.slot_state[v] = kSlotFree;
-    t.free_q[(t.fq_head + t.n_free) % t.N] = v;
+    t.slot_state[(size_t)v] = kSlotFree;
+    t.free_q[(size_t)wrap(t.fq_head + t.n_free, t.N)] = v;
     t.n_free++;
     return v;
 }
@@ -217,10 +240,17 @@ int write_rows(Table& t, int64_t n, const int64_t* idx, const void* const* col_s
         }
     }
     if (!any_kernel) return GEAR_OK;
-    // The slot list moves to the device once per chunk for all columns.
+    // The slot list moves to HBM once per chunk for all columns.
     for (int64_t off = 0; off < n; off += kStageRows) {
         const int64_t cnt = std::min(n - off, kStageRows);
-        hipError_t e = stage_indices(t, idx + off, cnt, s);
+        PinSlot ps;
+        hipError_t e = acquire_slot(t, ps);
+        if (e == hipSuccess) {
+            std::memcpy(ps.h_idx, idx + off, sizeof(int64_t) * (size_t)cnt);
+            hipLaunchKernelGGL(copy_list_kernel, dim3(blocks_for(cnt)), dim3(256), 0, s, ps.d_idx, cnt, t.stage_idx);
+            e = hipGetLastError();
+        }
+        if (e == hipSuccess) e = release_slot(t, ps, s);
         if (e != hipSuccess) return hip_fail(e, "staging slots");
         for (int c = 0; c < t.ncols && e == hipSuccess; c++) {
             if (!kernel_path[(size_t)c]) continue;
@@ -318,6 +348,11 @@ extern "C" int gear_allocate(gear_table* h, int64_t n, int64_t* idx_out, void* s
     if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_allocate: hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
     std::vector<int64_t> victims;
+    try {
+        victims.reserve((size_t)n);
+    } catch (const std::bad_alloc&) {
+        return fail(GEAR_E_NOMEM, "gear_allocate: host victim list");
+    }
     for (int64_t r = 0; r < n; r++) {
         // Pending stays below the maximum here, so a victim exists whenever one is needed.
         while (t->n_free == 0 || t->n_committed + t->n_pending >= t->max_selectable)
@@ -332,11 +367,14 @@ extern "C" int gear_allocate(gear_table* h, int64_t n, int64_t* idx_out, void* s
     // Victims become unselectable before the caller writes into any slot.
     for (size_t off = 0; off < victims.size(); off += (size_t)gear::kStageRows) {
         const int64_t cnt = (int64_t)std::min(victims.size() - off, (size_t)gear::kStageRows);
-        hipError_t e = gear::stage_indices(*t, victims.data() + off, cnt, s);
+        gear::PinSlot ps;
+        hipError_t e = gear::acquire_slot(*t, ps);
         if (e != hipSuccess) return hip_fail(e, "gear_allocate: staging victims");
-        hipLaunchKernelGGL(gear::evict_kernel, dim3(gear::blocks_for(cnt)), dim3(256), 0, s, t->stage_idx, cnt,
+        std::memcpy(ps.h_idx, victims.data() + off, sizeof(int64_t) * (size_t)cnt);
+        hipLaunchKernelGGL(gear::evict_kernel, dim3(gear::blocks_for(cnt)), dim3(256), 0, s, ps.d_idx, cnt,
                            t->priority, t->committed);
-        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "gear_allocate: launch");
+        if ((e = hipGetLastError()) == hipSuccess) e = gear::release_slot(*t, ps, s);
+        if (e != hipSuccess) return hip_fail(e, "gear_allocate: launch");
     }
     if (!victims.empty()) t->cdf_dirty = true;
     return GEAR_OK;
@@ -360,22 +398,33 @@ extern "C" int gear_commit(gear_table* h, int64_t n, const int64_t* idx, const u
     gear::DeviceGuard guard(t->device);
     if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_commit: hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
+    // Priorities in device or pinned memory are read in place; pageable
+    // ones go through the staging slot with the indices.
+    const bool prio_in_place = gear::device_readable(priorities);
     for (int64_t off = 0; off < n; off += gear::kStageRows) {
         const int64_t cnt = std::min(n - off, gear::kStageRows);
-        hipError_t e = gear::stage_indices(*t, idx + off, cnt, s);
-        if (e == hipSuccess)
-            e = hipMemcpyAsync(t->stage_prio, priorities + off, sizeof(uint32_t) * (size_t)cnt, hipMemcpyDefault, s);
+        gear::PinSlot ps;
+        hipError_t e = gear::acquire_slot(*t, ps);
         if (e != hipSuccess) return hip_fail(e, "gear_commit: staging");
-        const int64_t pos0 = (t->ord_head + t->n_committed) % t->N;
-        hipLaunchKernelGGL(gear::commit_kernel, dim3(gear::blocks_for(cnt)), dim3(256), 0, s, t->stage_idx,
-                           t->stage_prio, cnt, pos0, t->N, t->order, t->priority, t->committed);
-        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "gear_commit: launch");
+        std::memcpy(ps.h_idx, idx + off, sizeof(int64_t) * (size_t)cnt);
+        const uint32_t* p = priorities + off;
+        if (!prio_in_place) {
+            std::memcpy(ps.h_prio, p, sizeof(uint32_t) * (size_t)cnt);
+            p = ps.d_prio;
+        }
+        const int64_t pos0 = gear::wrap(t->ord_head + t->n_committed, t->N);
+        hipLaunchKernelGGL(gear::commit_kernel, dim3(gear::blocks_for(cnt)), dim3(256), 0, s, ps.d_idx, p, cnt, pos0,
+                           t->N, t->order, t->priority, t->committed);
+        if ((e = hipGetLastError()) == hipSuccess) e = gear::release_slot(*t, ps, s);
+        if (e != hipSuccess) return hip_fail(e, "gear_commit: launch");
+        int64_t pos = pos0;
         for (int64_t j = off; j < off + cnt; j++) {
             t->slot_state[(size_t)idx[j]] = gear::kSlotCommitted;
-            t->order_h[(size_t)((t->ord_head + t->n_committed) % t->N)] = (int32_t)idx[j];
-            t->n_committed++;
-            t->n_pending--;
+            t->order_h[(size_t)pos] = (int32_t)idx[j];
+            pos = gear::wrap(pos + 1, t->N);
         }
+        t->n_committed += cnt;
+        t->n_pending -= cnt;
     }
     t->next_seq += (uint64_t)n;
     t->cdf_dirty = true;

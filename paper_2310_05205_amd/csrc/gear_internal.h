@@ -34,6 +34,7 @@ constexpr int kTopkMaxK = GEAR_MAX_TOPK;
 // after the copy out of it has completed).
 constexpr int64_t kStageRows = 1 << 16;
 constexpr int kStageSlots = 4;
+constexpr int64_t kStageSlotBytes = kStageRows * (int64_t)(sizeof(int64_t) + sizeof(uint32_t));
 
 // Per-slot state of the index manager (host side).
 enum : uint8_t { kSlotFree = 0, kSlotPending = 1, kSlotCommitted = 2, kSlotMark = 3 };
@@ -85,11 +86,15 @@ struct Table {
     int64_t ord_head = 0, n_committed = 0, n_pending = 0;
     int32_t* order = nullptr;         // device copy of order_h (same positions)
     uint8_t* committed = nullptr;     // device [N]: 1 for committed slots
-    // Staging of host index and priority lists (every table).
-    int64_t* stage_idx = nullptr;     // device staging [kStageRows]
-    uint32_t* stage_prio = nullptr;   // device staging [kStageRows]
-    int64_t* pin_idx = nullptr;       // pinned host staging [kStageSlots][kStageRows]
-    hipEvent_t pin_free[kStageSlots] = {};  // recorded after the last copy out of each slot
+    // Staging of host index and priority lists (every table): a ring of
+    // pinned, mapped, coherent host slots that kernels read directly (small
+    // host-to-device copies left the GPU idle for about 25 us each), and an
+    // HBM copy of a slot list for the row scatter, which reads it once per
+    // workgroup.
+    int64_t* stage_idx = nullptr;     // device [kStageRows]
+    uint8_t* pin_host = nullptr;      // [kStageSlots][kStageSlotBytes]: int64 indices, then uint32 priorities
+    uint8_t* pin_dev = nullptr;       // the same ring's device address
+    hipEvent_t pin_free[kStageSlots] = {};  // recorded after the last kernel that reads each slot
     int pin_next = 0;                 // slot the next chunk uses
 
     uint64_t* topk_keys = nullptr;    // [kTopkMaxK] selected keys (p << 32 | ~slot), equal priorities in slot order

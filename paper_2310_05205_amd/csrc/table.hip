@@ -50,8 +50,7 @@ void free_table(Table* t) {
     if (!t) return;
     gear::free_index_manager(*t);
     (void)hipFree(t->stage_idx);
-    (void)hipFree(t->stage_prio);
-    if (t->pin_idx) (void)hipHostFree(t->pin_idx);
+    if (t->pin_host) (void)hipHostFree(t->pin_host);
     for (int k = 0; k < gear::kStageSlots; k++)
         if (t->pin_free[k]) (void)hipEventDestroy(t->pin_free[k]);
     for (int c = 0; c < t->ncols; c++) {
@@ -191,10 +190,14 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
     if ((e = dmalloc(&t->status, sizeof(uint32_t))) != hipSuccess) return oom("status word", e);
     // Staging for host index and priority lists (row writes, index manager).
     if ((e = dmalloc(&t->stage_idx, sizeof(int64_t) * gear::kStageRows)) != hipSuccess ||
-        (e = dmalloc(&t->stage_prio, sizeof(uint32_t) * gear::kStageRows)) != hipSuccess ||
-        (e = hipHostMalloc(reinterpret_cast<void**>(&t->pin_idx), sizeof(int64_t) * gear::kStageRows * gear::kStageSlots,
-                           hipHostMallocDefault)) != hipSuccess)
+        (e = hipHostMalloc(reinterpret_cast<void**>(&t->pin_host), (size_t)(gear::kStageSlotBytes * gear::kStageSlots),
+                           hipHostMallocMapped | hipHostMallocCoherent)) != hipSuccess)
         return oom("index staging", e);
+    {
+        void* d = nullptr;
+        if ((e = hipHostGetDevicePointer(&d, t->pin_host, 0)) != hipSuccess) return oom("a device view of the staging", e);
+        t->pin_dev = static_cast<uint8_t*>(d);
+    }
     for (int k = 0; k < gear::kStageSlots; k++)
         if ((e = hipEventCreateWithFlags(&t->pin_free[k], hipEventDisableTiming)) != hipSuccess) {
             free_table(t);
