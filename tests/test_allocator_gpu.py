@@ -112,8 +112,15 @@ def test_random_operation_sequences(removal, N, M, seed, residency):
                 m = int(rng.integers(1, len(pending) + 1))
                 pick = np.array([pending[j] for j in rng.permutation(len(pending))[:m]], dtype=np.int64)
                 prio = rng.integers(0, 50, size=m).astype(np.uint32)    # 0 commits an unselectable index
-                dev_prio = bool(rng.integers(0, 2))
-                t.commit(pick, torch.from_numpy(prio).to(cuda()) if dev_prio else prio)
+                # priorities from device memory and pinned host memory (read in
+                # place by the commit kernel) or pageable memory (staged)
+                src = int(rng.integers(0, 3))
+                if src == 0:
+                    t.commit(pick, torch.from_numpy(prio).to(cuda()))
+                elif src == 1:
+                    t.commit(pick, torch.from_numpy(prio.view(np.int32)).pin_memory())
+                else:
+                    t.commit(pick, prio)
                 assert store.commit(pick, prio) == oracle.OK
                 for i in pick:
                     pending.remove(int(i))
