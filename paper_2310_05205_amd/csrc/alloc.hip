@@ -60,17 +60,19 @@ __global__ void commit_kernel(const int64_t* __restrict__ idx, const uint32_t* _
 }
 
 // Row scatter: row r of a contiguous [n][row] source goes to slot idx[r] of
-// a column ([N][row]).  Rows of at least half a piece (kRowPiece elements):
-// a workgroup copies one piece of one row.  Smaller rows: a workgroup copies
-// the whole rows that fit in one piece, the destination of each row staged
-// in LDS.  Both the source (read once) and the table rows (not read soon)
-// are accessed non-temporally: measured on gfx950, that beats plain loads
-// and stores for this copy.  Pieces are small (one 16-byte element per lane
-// of a 64-lane workgroup, 1 KiB): writing 200 KB rows into a full table,
-// that reached 6.3 TB/s against 6.1 with 4 KiB and 5.6 with 16 KiB pieces.
+// a column ([N][row]).  Rows of at least half a piece: a workgroup copies
+// one piece of one row.  Smaller rows: a workgroup copies the whole rows that
+// fit in one piece, the destination of each row staged in LDS.  Both the
+// source (read once) and the table rows (not read soon) are accessed
+// non-temporally: measured on gfx950, that beats plain loads and stores for
+// this copy.  Pieces are small, 1 KiB for every element width (16 bytes per
+// lane of a 64-lane workgroup): writing 200 KB rows into a full table, that
+// reached 6.3 TB/s against 6.1 with 4 KiB and 5.6 with 16 KiB pieces.
 constexpr int kRowThreads = 64;
-constexpr int kRowUnroll = 1;
-constexpr int64_t kRowPiece = kRowThreads * kRowUnroll;
+template <typename V>
+constexpr int row_unroll() { return 16 / (int)sizeof(V); }  // elements per lane
+template <typename V>
+constexpr int64_t row_piece() { return (int64_t)kRowThreads * row_unroll<V>(); }  // elements per piece
 
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -78,34 +80,36 @@ template <typename V>
 __global__ __launch_bounds__(kRowThreads) void scatter_rows_kernel(const int64_t* __restrict__ idx,
                                                                    const V* __restrict__ src, V* __restrict__ dst,
                                                                    int64_t row_elems, int64_t pieces_per_row) {
+    constexpr int U = row_unroll<V>();
+    constexpr int64_t P = row_piece<V>();
     const int64_t q = blockIdx.x;
     const int64_t r = q / pieces_per_row;
-    const int64_t off = (q - r * pieces_per_row) * kRowPiece;
-    const int64_t len = row_elems - off < kRowPiece ? row_elems - off : kRowPiece;
+    const int64_t off = (q - r * pieces_per_row) * P;
+    const int64_t len = row_elems - off < P ? row_elems - off : P;
     const V* s = src + r * row_elems + off;
     V* d = dst + idx[r] * row_elems + off;
-    if (len == kRowPiece) {
-        V v[kRowUnroll];
+    if (len == P) {
+        V v[U];
 #pragma unroll
-        for (int k = 0; k < kRowUnroll; k++) v[k] = __builtin_nontemporal_load(s + threadIdx.x + k * kRowThreads);
+        for (int k = 0; k < U; k++) v[k] = __builtin_nontemporal_load(s + threadIdx.x + k * kRowThreads);
 #pragma unroll
-        for (int k = 0; k < kRowUnroll; k++) __builtin_nontemporal_store(v[k], d + threadIdx.x + k * kRowThreads);
+        for (int k = 0; k < U; k++) __builtin_nontemporal_store(v[k], d + threadIdx.x + k * kRowThreads);
     } else {
         for (int64_t e = threadIdx.x; e < len; e += kRowThreads)
             __builtin_nontemporal_store(__builtin_nontemporal_load(s + e), d + e);
     }
 }
 
-// Rows of fewer than kRowPiece / 2 elements: workgroup q copies rows
+// Rows of fewer than half a piece: workgroup q copies rows
 // q*rpw .. q*rpw + rpw - 1.  Element e of that range is row e / row_elems,
 // computed as (e * magic) >> 32 with magic = ceil(2^32 / row_elems), exact
-// for e < kRowPiece.
+// for e below a piece (at most 1024 elements).
 template <typename V>
 __global__ __launch_bounds__(kRowThreads) void scatter_small_rows_kernel(const int64_t* __restrict__ idx, int64_t n,
                                                                          const V* __restrict__ src,
                                                                          V* __restrict__ dst, int64_t row_elems,
                                                                          int rpw, uint64_t magic) {
-    __shared__ int64_t s_dst[kRowPiece];
+    __shared__ int64_t s_dst[row_piece<V>()];
     const int64_t r0 = (int64_t)blockIdx.x * rpw;
     const int nr = (int)(n - r0 < rpw ? n - r0 : rpw);
     for (int i = threadIdx.x; i < nr; i += kRowThreads) s_dst[i] = idx[r0 + i] * row_elems;
@@ -122,19 +126,28 @@ __global__ __launch_bounds__(kRowThreads) void scatter_small_rows_kernel(const i
 template <typename V>
 hipError_t launch_rows(const int64_t* d_idx, int64_t n, const uint8_t* src, uint8_t* dst, int64_t row_bytes,
                        hipStream_t s) {
+    constexpr int64_t P = row_piece<V>();
     const int64_t row_elems = row_bytes / (int64_t)sizeof(V);
-    if (row_elems * 2 < kRowPiece) {
-        const int rpw = (int)(kRowPiece / row_elems);
+    if (row_elems * 2 < P) {
+        const int rpw = (int)(P / row_elems);
         const uint64_t magic = ((1ull << 32) + (uint64_t)row_elems - 1) / (uint64_t)row_elems;
         hipLaunchKernelGGL(scatter_small_rows_kernel<V>, dim3((unsigned)((n + rpw - 1) / rpw)), dim3(kRowThreads), 0,
                            s, d_idx, n, reinterpret_cast<const V*>(src), reinterpret_cast<V*>(dst), row_elems, rpw,
                            magic);
         return hipGetLastError();
     }
-    const int64_t ppr = (row_elems + kRowPiece - 1) / kRowPiece;
-    hipLaunchKernelGGL(scatter_rows_kernel<V>, dim3((unsigned)(n * ppr)), dim3(kRowThreads), 0, s, d_idx,
-                       reinterpret_cast<const V*>(src), reinterpret_cast<V*>(dst), row_elems, ppr);
-    return hipGetLastError();
+    // One workgroup per piece; rows are split over launches so that no grid
+    // exceeds 2^31 - 1 workgroups.
+    const int64_t ppr = (row_elems + P - 1) / P;
+    const int64_t rows_per_launch = ppr >= 0x7FFFFFFF ? 1 : 0x7FFFFFFF / ppr;
+    for (int64_t r0 = 0; r0 < n; r0 += rows_per_launch) {
+        const int64_t m = n - r0 < rows_per_launch ? n - r0 : rows_per_launch;
+        hipLaunchKernelGGL(scatter_rows_kernel<V>, dim3((unsigned)(m * ppr)), dim3(kRowThreads), 0, s, d_idx + r0,
+                           reinterpret_cast<const V*>(src + r0 * row_bytes), reinterpret_cast<V*>(dst), row_elems, ppr);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 // Whether a kernel on the table's device can read `p` (device memory, or
