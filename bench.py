@@ -241,6 +241,38 @@ def host_link_extras(t, w, idx, start, outs, dev):
                                    "per column; median of 3 batches"}}
 
 
+def torch_context(t, w, dev):
+    """The same selection done with PyTorch's own GPU operators, on a copy of
+    the table's priorities, timed with events over 20 calls: torch.multinomial
+    (weighted draws with replacement, fp32 weights) for prioritized
+    selection, torch.topk for TopK.  Context only: neither reproduces the
+    exact draws or tie order, and neither is the baseline."""
+    import torch
+
+    p = torch.from_numpy(t.priorities().astype("int64")).to(dev)
+    strat = w.strategies[0]
+    if strat == 3:
+        x = p.to(torch.float32)
+        fn = lambda: torch.multinomial(x, w.B, replacement=True)
+        name = "torch_multinomial_us"
+    elif strat == 4:
+        fn = lambda: torch.topk(p, w.B)
+        name = "torch_topk_us"
+    else:
+        return None
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(20):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return {name: round(e0.elapsed_time(e1) * 1e3 / 20, 2),
+            "note": "PyTorch operator on the same priorities, for scale; the GPU select is stages_ms.select"}
+
+
 def cpu_baseline(w, target_s, global_min=False):
     """The oracle, single-threaded, on a bounded sample: repeated steps of
     the same workload (select over all N priorities, IS weights, collection
@@ -641,6 +673,8 @@ def main():
                 "kernel": "collect_kernel", "algorithmic_bytes_per_launch": alg_bytes,
                 "avg_launch_ms": round(col_ms, 5)}
 
+    context = torch_context(t, w, dev) if strategy in (gear.GEAR_PRIORITIZED, gear.GEAR_TOPK) else None
+
     link = None
     if host_table and outs:
         link = host_link_extras(t, w, idx, start, outs, dev)
@@ -676,6 +710,8 @@ def main():
     }
     if link is not None:
         line["host_link"] = link
+    if context is not None:
+        line["torch_context"] = context
     t.close()
     print(json.dumps(line), flush=True)
 
