@@ -86,3 +86,18 @@ def test_product_has_no_oracle_or_fallback():
                     src = f.read()
                 assert "import oracle" not in src and "from oracle" not in src, fn
                 assert "oracle_" not in src, fn
+
+
+def test_missing_library_fails_loudly():
+    """Without a built libgear.so the binding raises; there is no fallback."""
+    from paper_2310_05205_amd import gear
+    saved_path, saved_lib = gear.LIB_PATH, gear._lib
+    try:
+        gear.LIB_PATH = os.path.join(ROOT, "_no_such_dir", "libgear.so")
+        gear._lib = None
+        with pytest.raises(RuntimeError, match="not built"):
+            gear.lib()
+        with pytest.raises(RuntimeError, match="not built"):
+            gear.gear_table_create([4], 16, 2)
+    finally:
+        gear.LIB_PATH, gear._lib = saved_path, saved_lib
