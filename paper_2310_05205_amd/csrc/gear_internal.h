@@ -29,9 +29,10 @@ constexpr int kTopkBins = 4096;       // bins of one TopK digit pass (12-bit dig
 constexpr int kTopkStateWords = 32;   // TopK selection states after 0 .. 3 digit passes
 constexpr int kTopkRankBlock = 512;    // keys one TopK rank workgroup compares against
 constexpr int kTopkMaxK = GEAR_MAX_TOPK;
-// Index manager: index lists move to the device in chunks of this many,
-// through a ring of this many pinned host buffers (a buffer is refilled only
-// after the copy out of it has completed).
+// Host index and priority lists (row writes, allocation, commits) are
+// handled in chunks of kStageRows entries, through a ring of kStageSlots
+// pinned, mapped slots that kernels read in place (a slot is refilled only
+// after its last reader has run).
 constexpr int64_t kStageRows = 1 << 16;
 constexpr int kStageSlots = 4;
 constexpr int64_t kStageSlotBytes = kStageRows * (int64_t)(sizeof(int64_t) + sizeof(uint32_t));
