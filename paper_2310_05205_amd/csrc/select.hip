@@ -262,8 +262,20 @@ __global__ __launch_bounds__(256) void is_weights_kernel(int32_t B, double beta,
     __shared__ uint32_t s_min[4];
     const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const uint32_t pb = b < B ? reinterpret_cast<const uint32_t*>(w)[b] : 0u;
+    // Eight minima per thread are loaded before any is compared, so one
+    // memory round trip covers the search's largest grid.
+    constexpr int kMinPerThread = 8;
     uint32_t m = 0xFFFFFFFFu;
-    for (int k = threadIdx.x; k < search_grid; k += blockDim.x) m = wg_min[k] < m ? wg_min[k] : m;
+    for (int k0 = threadIdx.x; k0 < search_grid; k0 += blockDim.x * kMinPerThread) {
+        uint32_t v[kMinPerThread];
+#pragma unroll
+        for (int u = 0; u < kMinPerThread; u++) {
+            const int k = k0 + u * (int)blockDim.x;
+            v[u] = k < search_grid ? wg_min[k] : 0xFFFFFFFFu;
+        }
+#pragma unroll
+        for (int u = 0; u < kMinPerThread; u++) m = v[u] < m ? v[u] : m;
+    }
 #pragma unroll
     for (int d = 32; d >= 1; d >>= 1) {
         const uint32_t o = __shfl_xor(m, d);
