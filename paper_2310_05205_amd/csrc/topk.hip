@@ -18,8 +18,8 @@
 //
 //   topk_hist_kernel    (x3) a workgroup histograms one digit of the keys
 //                       whose higher digits match the ones chosen so far,
-//                       in LDS (the lanes of a wave that share the first
-//                       lane's bin add with one atomic), adds its
+//                       in eight LDS copies of the histogram (a thread adds
+//                       into copy thread mod 8), sums the copies, adds its
 //                       bins into the pass's global histogram and stores the
 //                       suffix sums of its own histogram.
 //   topk_compact_kernel finishes the threshold; the stored suffix sums give
@@ -50,6 +50,13 @@ constexpr int kBins = kTopkBins;
 constexpr int kDigit = 12;
 constexpr int kKeyBits = 36;
 constexpr int kPasses = kKeyBits / kDigit;
+// LDS copies of a digit histogram.  With skewed priorities most lanes of a
+// wave add into the same few bins, and LDS serialises atomics of one
+// instruction that hit one address; spreading the lanes over eight copies
+// (rows 4 words longer than a histogram, so a bin's copies sit in
+// different banks) cuts those conflicts eightfold: 131 KB of LDS.
+constexpr int kLdsCopies = 8;
+constexpr int kLdsStride = kBins + 4;
 
 constexpr uint32_t kAll = 1u;           // fewer than K candidates: take every one
 constexpr uint32_t kDone = 2u;          // the threshold is fully determined
@@ -189,7 +196,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_hist_kernel(const uint32_t*
                                                                  uint32_t* __restrict__ hist,
                                                                  uint32_t* __restrict__ local,
                                                                  TopkState* __restrict__ states) {
-    __shared__ __align__(16) uint32_t sh[kBins];
+    __shared__ __align__(16) uint32_t sh[kLdsCopies * kLdsStride];
     __shared__ DeriveShared dsh;
     __shared__ uint64_t s_wt[kTopkWaves];
     TopkState prev = initial_state(K);
@@ -206,7 +213,9 @@ __global__ __launch_bounds__(kTopkThreads) void topk_hist_kernel(const uint32_t*
     wg_range(N, chunk, lo, hi);
     uint32_t v[kVec][4];
     load_batch(prio, lo, hi, v);
-    for (int b = threadIdx.x; b < kBins; b += kTopkThreads) sh[b] = 0;
+    for (int b = threadIdx.x * 4; b < kLdsCopies * kLdsStride; b += kTopkThreads * 4)
+        *reinterpret_cast<uint4*>(&sh[b]) = make_uint4(0u, 0u, 0u, 0u);
+    uint32_t* const copy = sh + (threadIdx.x % kLdsCopies) * kLdsStride;
     __syncthreads();
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     for (int64_t base = lo; base < hi; base += kBatch) {
@@ -217,21 +226,9 @@ __global__ __launch_bounds__(kTopkThreads) void topk_hist_kernel(const uint32_t*
             for (int q = 0; q < 4; q++) {
                 const uint32_t p = v[k][q];
                 const uint64_t key = order_key(p);
-                bool left = p != 0u && (pass == 0 || (key >> prev_shift) == prev.prefix);
+                const bool counted = p != 0u && (pass == 0 || (key >> prev_shift) == prev.prefix);
                 const uint32_t bin = (uint32_t)(key >> shift) & (uint32_t)(kBins - 1);
-                // The lanes that share the first counted lane's bin (most
-                // lanes, when the priorities are skewed) add once; the rest
-                // add one each.  A second or third such round measured
-                // slower than the atomics it saves.
-                const uint64_t vm = __ballot(left);
-                if (vm != 0) {
-                    const int first = __ffsll((long long)vm) - 1;
-                    const uint32_t b0 = (uint32_t)__builtin_amdgcn_readlane((int)bin, first);
-                    const uint64_t m = __ballot(left && bin == b0);
-                    if (lane == first) atomicAdd(&sh[b0], (uint32_t)__popcll(m));
-                    left = left && bin != b0;
-                }
-                if (left) atomicAdd(&sh[bin], 1u);
+                if (counted) atomicAdd(&copy[bin], 1u);
             }
         }
     }
@@ -239,7 +236,15 @@ __global__ __launch_bounds__(kTopkThreads) void topk_hist_kernel(const uint32_t*
     // Add into the global histogram; store this workgroup's suffix sums
     // (S[b] = its keys in bins >= b) for the offsets of the compaction.
     const int b0 = first_bin();
-    const uint4 h = *reinterpret_cast<const uint4*>(&sh[b0]);
+    uint4 h = make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+    for (int c = 0; c < kLdsCopies; c++) {
+        const uint4 x = *reinterpret_cast<const uint4*>(&sh[c * kLdsStride + b0]);
+        h.x += x.x;
+        h.y += x.y;
+        h.z += x.z;
+        h.w += x.w;
+    }
     uint32_t* out = hist + pass * kBins + b0;
     if (h.x) atomicAdd(out + 0, h.x);
     if (h.y) atomicAdd(out + 1, h.y);
