@@ -120,7 +120,9 @@ def calibrate():
 def ceilings():
     """HBM rates of plain torch kernels on 8 GiB buffers (no gather, no
     replay): a read-only reduction, a fill, and an elementwise copy.  They
-    bound what a kernel that reads and writes HBM can reach on this device."""
+    bound what a kernel that reads and writes HBM can reach on this device.
+    Then plain copies of the gather's own sizes, which show what launch,
+    ramp and drain cost at those sizes."""
     import torch
     n = (8 << 30) // 4
     a = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -143,8 +145,36 @@ def ceilings():
         ms = hev.elapsed_ms(e0, e1) / 10
         out[name] = {"GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1), "ms": round(ms, 4),
                      "frac_of_8TB/s": round(nbytes / (ms * 1e-3) / 8e12, 4)}
+    # Copies of the gather's own sizes, from and to a fresh 1 GiB region each
+    # time (eight regions, more than the 256 MB last-level cache holds), as
+    # the gather reads windows no earlier step touched: the DT-shaped whole
+    # trajectories (51.2 MB each way) and the MAT windows (277.9 MB each way).
+    region = (1 << 30) // 4
+    sized = {}
+    for label, nbytes in (("dt-full 51.2 MB", 51_200_000), ("mat 277.9 MB", 277_872_640)):
+        m = nbytes // 4
+        for kind in ("runtime copy", "elementwise"):
+            def run(k, kind=kind, m=m):
+                src = a[(k % 8) * region:(k % 8) * region + m]
+                dst = b[((k + 3) % 8) * region:((k + 3) % 8) * region + m]
+                if kind == "runtime copy":
+                    dst.copy_(src)
+                else:
+                    torch.neg(src, out=dst)
+            for k in range(3):
+                run(k)
+            e0, e1 = hev.create(), hev.create()
+            hev.record(e0, sh)
+            reps = 16
+            for k in range(reps):
+                run(k)
+            hev.record(e1, sh)
+            torch.cuda.synchronize()
+            ms = hev.elapsed_ms(e0, e1) / reps
+            sized["%s, %s" % (label, kind)] = {"GB/s": round(2 * nbytes / (ms * 1e-3) / 1e9, 1), "us": round(ms * 1e3, 2),
+                                               "frac_of_8TB/s": round(2 * nbytes / (ms * 1e-3) / 8e12, 4)}
     hev.close()
-    print(json.dumps({"ceilings": out, "bytes_per_buffer": n * 4}))
+    print(json.dumps({"ceilings": out, "bytes_per_buffer": n * 4, "gather_sized_copies": sized}))
 
 
 def source_sha(path):
