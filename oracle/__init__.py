@@ -50,8 +50,10 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        build()
-        L = ctypes.CDLL(_LIB)
+        # ORACLE_LIB names another build of oracle.c to load instead; the
+        # mutation test loads deliberately broken builds through it.
+        path = os.environ.get("ORACLE_LIB") or build()
+        L = ctypes.CDLL(path)
         u64, i64, i32, u32p = ctypes.c_uint64, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
         vp = ctypes.c_void_p
         L.oracle_mix64.argtypes = [u64]; L.oracle_mix64.restype = u64
