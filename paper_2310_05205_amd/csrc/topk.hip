@@ -22,8 +22,10 @@
 //                       into copy thread mod 8), sums the copies, adds its
 //                       bins into the pass's global histogram and stores the
 //                       suffix sums of its own histogram.
-//   topk_compact_kernel finishes the threshold; the stored suffix sums give
-//                       every workgroup's count above and at it, hence this
+//   topk_compact_kernel finishes the threshold and turns it into a range of
+//                       priorities, so a key is classified with two integer
+//                       compares; the stored suffix sums give every
+//                       workgroup's count above and at it, hence this
 //                       workgroup's output offsets; one scan per batch of
 //                       loads orders its keys by slot.  It writes
 //                       (p << 32 | ~slot) of every slot above the threshold
@@ -264,16 +266,30 @@ __global__ __launch_bounds__(kTopkThreads) void topk_hist_kernel(const uint32_t*
     *reinterpret_cast<uint4*>(local + ((size_t)pass * kTopkMaxGrid + blockIdx.x) * kBins + b0) = S;
 }
 
-// Above / at the threshold of a decided state.
-__device__ __forceinline__ void classify(uint32_t p, const TopkState& st, int shift, bool& gt, bool& eq) {
+// The smallest priority p >= 1 whose order key is at least X, or 2^32 if
+// there is none.  Keys of the priorities with leading one at bit e are
+// (e << 31) | (r << (31 - e)) for p = 2^e + r, increasing in r.
+__device__ __forceinline__ uint64_t first_priority_with_key(uint64_t X) {
+    const uint64_t e = X >> 31;
+    if (e > 31) return 1ull << 32;
+    const uint64_t m = X & 0x7FFFFFFFull;
+    const int sh = 31 - (int)e;
+    const uint64_t r = (m + (1ull << sh) - 1) >> sh;
+    if (r < (1ull << e)) return (1ull << e) + r;
+    return 2ull << e;  // the first priority of the next leading-one position (2^32: none)
+}
+
+// A decided state as a priority range: keys at the threshold are the
+// priorities in [lo, hi), keys above it those from hi on (the order key is
+// increasing in the priority).  Taking every candidate is lo = hi = 1.
+__device__ __forceinline__ void threshold_range(const TopkState& st, uint64_t& lo, uint64_t& hi) {
     if (st.flags & kAll) {
-        gt = p != 0u;
-        eq = false;
-    } else {
-        const uint64_t k = order_key(p) >> shift;
-        gt = p != 0u && k > st.prefix;
-        eq = p != 0u && k == st.prefix;
+        lo = hi = 1;
+        return;
     }
+    const int shift = state_shift(st);
+    lo = first_priority_with_key(st.prefix << shift);
+    hi = first_priority_with_key((st.prefix + 1) << shift);
 }
 
 // Workgroup g's keys above and at the threshold, from its suffix sums of
@@ -306,9 +322,9 @@ __global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(const uint32
                                                                     uint64_t* __restrict__ keys,
                                                                     uint32_t* __restrict__ rank) {
     __shared__ DeriveShared dsh;
-    __shared__ uint64_t s_pre[kVec * kTopkWaves];  // per (load, wave): packed counts, then their prefix
+    __shared__ uint32_t s_pre[kVec * kTopkWaves];  // per (load, wave): packed counts, then their prefix
     __shared__ uint64_t s_base[5];                 // above base, at base, total above, own above, own at
-    __shared__ uint64_t s_batch;                   // packed counts of the whole batch
+    __shared__ uint32_t s_batch;                   // packed counts of the whole batch
     const uint4 row = load_row(hist, kPasses - 1);
     const TopkState stored = states[kPasses - 1];
     int64_t lo, hi;
@@ -319,7 +335,9 @@ __global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(const uint32
     if (blockIdx.x == 0 && threadIdx.x == 0) states[kPasses] = st;  // the final state, for rank and emit
     // The rank kernel accumulates into rank: start it at zero.
     for (int k = blockIdx.x * kTopkThreads + threadIdx.x; k < (int)K; k += grid * kTopkThreads) rank[k] = 0u;
-    const int shift = state_shift(st);
+    uint64_t p_lo, p_hi;
+    threshold_range(st, p_lo, p_hi);
+    const uint64_t p_width = p_hi - p_lo;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     if (wave == 0) {
@@ -355,7 +373,8 @@ __global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(const uint32
     if (s_base[3] == 0 && (s_base[4] == 0 || run_eq >= e_need)) return;
     for (int64_t base = lo; base < hi; base += kBatch) {
         if (base != lo) load_batch(prio, base, hi, v);
-        uint64_t c[kVec], incl[kVec];
+        // Counts packed as above | at << 16: a batch holds at most kBatch keys.
+        uint32_t c[kVec], incl[kVec];
         uint32_t cls[kVec];  // per element: bit q above, bit 4 + q at
 #pragma unroll
         for (int k = 0; k < kVec; k++) {
@@ -363,19 +382,20 @@ __global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(const uint32
             cls[k] = 0;
 #pragma unroll
             for (int q = 0; q < 4; q++) {
-                bool gt, eq;
-                classify(v[k][q], st, shift, gt, eq);
-                c[k] += (uint64_t)gt | ((uint64_t)eq << 32);
+                const uint64_t p = v[k][q];
+                const bool gt = p >= p_hi;
+                const bool eq = p - p_lo < p_width;
+                c[k] += (uint32_t)gt | ((uint32_t)eq << 16);
                 cls[k] |= (gt ? 1u << q : 0u) | (eq ? 16u << q : 0u);
             }
-            incl[k] = wave_inclusive_scan(c[k]);
+            incl[k] = wave_inclusive_scan32(c[k]);
             if (lane == 63) s_pre[k * kTopkWaves + wave] = incl[k];
         }
         __syncthreads();
         if (wave == 0) {
             // Exclusive scan of the kVec x kTopkWaves wave counts in (load, wave) order.
-            const uint64_t a = s_pre[lane];
-            const uint64_t s = wave_inclusive_scan(a);
+            const uint32_t a = s_pre[lane];
+            const uint32_t s = wave_inclusive_scan32(a);
             s_pre[lane] = s - a;
             if (lane == 63) s_batch = s;
         }
@@ -383,9 +403,9 @@ __global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(const uint32
 #pragma unroll
         for (int k = 0; k < kVec; k++) {
             if (cls[k] == 0) continue;
-            const uint64_t off = s_pre[k * kTopkWaves + wave] + incl[k] - c[k];
-            uint64_t og = run_gt + (uint32_t)off;  // output position of this lane's first key above
-            uint64_t oe = run_eq + (off >> 32);    // slot-order rank of its first key at the threshold
+            const uint32_t off = s_pre[k * kTopkWaves + wave] + incl[k] - c[k];
+            uint64_t og = run_gt + (off & 0xFFFFu);  // output position of this lane's first key above
+            uint64_t oe = run_eq + (off >> 16);      // slot-order rank of its first key at the threshold
             const int64_t e0 = base + ((int64_t)k * kTopkThreads + threadIdx.x) * 4;
 #pragma unroll
             for (int q = 0; q < 4; q++) {
@@ -403,13 +423,14 @@ __global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(const uint32
                 }
             }
         }
-        const uint64_t tb = s_batch;
-        run_gt += (uint32_t)tb;
-        run_eq += tb >> 32;
+        const uint32_t tb = s_batch;
+        run_gt += tb & 0xFFFFu;
+        run_eq += tb >> 16;
         __syncthreads();  // s_pre and s_batch are rewritten by the next batch
     }
 }
 static_assert(kVec * kTopkWaves == 64, "one lane of wave 0 per (load, wave) count");
+static_assert(kBatch < 65536, "a batch's counts fit the 16-bit fields");
 
 // Number of selected keys: K, or every candidate when there are fewer.
 __device__ __forceinline__ int selected(const TopkState& st, int32_t K) {

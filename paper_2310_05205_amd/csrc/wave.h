@@ -41,6 +41,22 @@ __device__ __forceinline__ uint64_t wave_inclusive_scan(uint64_t v) {
     return v;
 }
 
+// The same scan on 32-bit values.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp32(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROW_MASK, 0xf, false);
+}
+
+__device__ __forceinline__ uint32_t wave_inclusive_scan32(uint32_t v) {
+    v += dpp32<0x111, 0xf>(v);  // row_shr:1
+    v += dpp32<0x112, 0xf>(v);  // row_shr:2
+    v += dpp32<0x114, 0xf>(v);  // row_shr:4
+    v += dpp32<0x118, 0xf>(v);  // row_shr:8
+    v += dpp32<0x142, 0xa>(v);  // row_bcast:15 into rows 1 and 3
+    v += dpp32<0x143, 0xc>(v);  // row_bcast:31 into rows 2 and 3
+    return v;
+}
+
 // Value of v in lane `src` (src is the same in every lane).
 __device__ __forceinline__ uint64_t read_lane(uint64_t v, int src) {
     const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, src);
