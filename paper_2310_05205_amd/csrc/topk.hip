@@ -220,17 +220,35 @@ __global__ __launch_bounds__(kTopkThreads) void topk_hist_kernel(const uint32_t*
     uint32_t* const copy = sh + (threadIdx.x % kLdsCopies) * kLdsStride;
     __syncthreads();
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    // Pass 0 counts every non-zero priority; its digit is the leading-one
+    // position and the 7 bits below it, computed in 32 bits.  A zero
+    // priority adds into one of the row's unused padding words instead, so
+    // the loop has no branch.
+    const uint32_t pad = (uint32_t)kBins + ((threadIdx.x >> 3) & 3u);
     for (int64_t base = lo; base < hi; base += kBatch) {
         if (base != lo) load_batch(prio, base, hi, v);
+        if (pass == 0) {
 #pragma unroll
-        for (int k = 0; k < kVec; k++) {
+            for (int k = 0; k < kVec; k++) {
 #pragma unroll
-            for (int q = 0; q < 4; q++) {
-                const uint32_t p = v[k][q];
-                const uint64_t key = order_key(p);
-                const bool counted = p != 0u && (pass == 0 || (key >> prev_shift) == prev.prefix);
-                const uint32_t bin = (uint32_t)(key >> shift) & (uint32_t)(kBins - 1);
-                if (counted) atomicAdd(&copy[bin], 1u);
+                for (int q = 0; q < 4; q++) {
+                    const uint32_t p = v[k][q];
+                    const uint32_t z = __clz(p | 1u);                    // 31 - leading-one position
+                    const uint32_t d = ((31u - z) << 7) | ((p << z) >> 24 & 0x7Fu);
+                    atomicAdd(&copy[p != 0u ? d : pad], 1u);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < kVec; k++) {
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    const uint32_t p = v[k][q];
+                    const uint64_t key = order_key(p);
+                    const bool counted = p != 0u && (key >> prev_shift) == prev.prefix;
+                    const uint32_t bin = (uint32_t)(key >> shift) & (uint32_t)(kBins - 1);
+                    if (counted) atomicAdd(&copy[bin], 1u);
+                }
             }
         }
     }
