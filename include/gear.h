@@ -21,7 +21,14 @@
  *     released some victims); the table should then be closed.
  *   - `stream` is a hipStream_t passed as void*; NULL means the null stream.
  *     Every device-side effect is enqueued on `stream` and is asynchronous
- *     to the host; only gear_table_sync() blocks.
+ *     to the host.  Calls do not wait for the device, except:
+ *     gear_table_sync(), which exists to; gear_table_create,
+ *     gear_table_use_allocator and gear_table_destroy, which synchronise the
+ *     device at set-up and tear-down; calls that pass an index list through
+ *     the table's four pinned staging slots (gear_allocate, gear_commit,
+ *     gear_write_rows, and gear_insert with an index manager), which wait
+ *     only when every slot is still being read by earlier work; and copies
+ *     from pageable host memory, which HIP performs synchronously.
  *   - Pointers named d_* are device memory (hipMalloc, or a torch CUDA
  *     tensor's data pointer) on the table's device.  They are owned by the
  *     caller and must stay valid until the enqueued work has completed.
