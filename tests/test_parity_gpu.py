@@ -451,3 +451,48 @@ def test_topk_rejects_oversized_batch():
         assert e.value.code == gear.GEAR_E_INVAL
     finally:
         t.close()
+
+
+def _boundary_priorities(rng, N):
+    """Priorities clustered around powers of two (2^e - 2 .. 2^e + 2 for
+    several e, and the top of the 32-bit range), where the TopK threshold's
+    digit prefix changes leading-one position, plus uniform filler.  Returns
+    the priorities and the cluster values."""
+    centres = [1 << e for e in (1, 2, 7, 8, 9, 12, 20, 24, 31)]
+    cluster = np.array(sorted({c + d for c in centres for d in (-2, -1, 0, 1, 2)} |
+                              {1, 2, 3, 0xFFFFFFFE, 0xFFFFFFFF}), dtype=np.uint64)
+    p = np.where(rng.random(N) < 0.7, cluster[rng.integers(0, cluster.size, N)],
+                 rng.integers(1, 1 << 32, N, dtype=np.uint64))
+    p[rng.random(N) < 0.05] = 0
+    return p.astype(np.uint32), cluster.astype(np.uint32)
+
+
+def test_topk_threshold_at_exponent_boundaries():
+    """The K-th largest priority placed at and next to powers of two: K is
+    each cluster value's first and last position in descending order, so the
+    threshold falls on every side of every boundary."""
+    rng = np.random.default_rng(20)
+    N, T = 12000, 2  # every non-zero priority lies within the first GEAR_MAX_TOPK places
+    p, cluster = _boundary_priorities(rng, N)
+    t = gear.Table([1], capacity=N, T=T, residency=gear.GEAR_DEVICE, device=0)
+    try:
+        t.insert([np.zeros((N, T), np.uint8)], p)
+        order = np.argsort(-p.astype(np.int64), kind="stable")
+        desc = p[order]
+        ks = set()
+        for v in cluster:
+            pos = np.nonzero(desc == v)[0]
+            if pos.size == 0:
+                continue
+            ks.update({int(pos[0]) + 1, int(pos[-1]) + 1, int(pos[-1]) + 2})
+        ks = sorted(k for k in ks if 1 <= k <= gear.GEAR_MAX_TOPK)
+        say("TopK at %d thresholds around powers of two" % len(ks))
+        for K in ks:
+            idx, start, wt = t.select(gear.GEAR_TOPK, K, 1, 7, 0.0, weights=True)
+            st, oidx, ostart, ow = oracle.select(oracle.TOPK, p, N, T, K, 1, 7, 0.0, True)
+            np.testing.assert_array_equal(host(idx), oidx, err_msg="K=%d" % K)
+            np.testing.assert_array_equal(host(start), ostart)
+            np.testing.assert_array_equal(host(wt), ow)
+            assert t.sync() == (0 if st == oracle.OK else gear.GEAR_STATUS_NO_WEIGHT)
+    finally:
+        t.close()
