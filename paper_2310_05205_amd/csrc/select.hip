@@ -23,6 +23,12 @@
 //                  smallest i with C_i > r for the inclusive prefix C over
 //                  all priorities: the binary-search answer.
 //
+// Small tables (N <= kSmallN, B <= kSmallMaxB, sum tree not kept across
+// updates) take one launch instead: small_select_kernel, one workgroup,
+// forms the inclusive prefix C of all N priorities in LDS with a block scan,
+// finds each draw's slot as the smallest i with C_i > r by bisection over
+// C, and computes the IS weights, all in one launch.
+//
 // FIFO, LIFO and uniform selection are one thread per draw.
 #include "gear_internal.h"
 #include "wave.h"
@@ -289,6 +295,99 @@ __global__ __launch_bounds__(256) void is_weights_kernel(int32_t B, double beta,
     w[b] = (pb == 0u || m == 0u) ? 0.0f : (float)pow((double)m / (double)pb, beta);
 }
 
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallPerThread = (int)(kSmallN / kSmallThreads);  // consecutive priorities per thread
+static_assert(kSmallN % (4 * kSmallThreads) == 0, "whole 16-byte loads per thread");
+
+// LDS position of prefix entry e: one pad word after every run of
+// kSmallPerThread entries, so that the lanes of a wave, each writing its own
+// consecutive run, fall in different banks.
+__device__ __forceinline__ int64_t small_pos(int64_t e) { return e + e / kSmallPerThread; }
+
+// want_w: also compute weights (the selected priority waits in w[b] as
+// uint32 bits, as in the multi-launch path).  global_min: normalise by the
+// smallest non-zero priority of the table instead of the batch's.
+__global__ __launch_bounds__(kSmallThreads) void small_select_kernel(const uint32_t* __restrict__ prio, int64_t N,
+                                                                     int32_t B, uint64_t span, uint64_t seed,
+                                                                     int want_w, int global_min, double beta,
+                                                                     uint32_t* status, int64_t* __restrict__ idx,
+                                                                     int32_t* __restrict__ start,
+                                                                     float* __restrict__ w) {
+    __shared__ uint64_t C[kSmallN + kSmallN / kSmallPerThread];
+    __shared__ uint64_t s_wave[kSmallThreads / 64];
+    __shared__ uint32_t s_min[kSmallThreads / 64];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int64_t e0 = (int64_t)t * kSmallPerThread;
+    uint32_t v[kSmallPerThread];
+#pragma unroll
+    for (int k = 0; k < kSmallPerThread; k += 4) {
+        if (e0 + k + 4 <= N) {
+            const uint4 x = *reinterpret_cast<const uint4*>(prio + e0 + k);
+            v[k] = x.x; v[k + 1] = x.y; v[k + 2] = x.z; v[k + 3] = x.w;
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; q++) v[k + q] = e0 + k + q < N ? prio[e0 + k + q] : 0u;
+        }
+    }
+    // Block-wide inclusive scan: this thread's run, then the waves in order.
+    uint64_t run = 0;
+    uint32_t pmin = 0xFFFFFFFFu;  // smallest non-zero priority of this thread's run
+#pragma unroll
+    for (int k = 0; k < kSmallPerThread; k++) {
+        run += v[k];
+        pmin = (v[k] != 0u && v[k] < pmin) ? v[k] : pmin;
+    }
+    const uint64_t incl = wave_inclusive_scan(run);
+    if (lane == 63) s_wave[wave] = incl;
+    __syncthreads();
+    uint64_t acc = incl - run;
+    for (int q = 0; q < wave; q++) acc += s_wave[q];
+#pragma unroll
+    for (int k = 0; k < kSmallPerThread; k++) {
+        acc += v[k];
+        if (e0 + k < N) C[small_pos(e0 + k)] = acc;
+    }
+    __syncthreads();
+    const uint64_t S = C[small_pos(N - 1)];
+    uint32_t m = 0xFFFFFFFFu;  // smallest selected priority (or of the table)
+    for (int64_t b = t; b < B; b += kSmallThreads) {
+        if (S == 0) {
+            idx[b] = -1;
+            start[b] = 0;
+            if (want_w) reinterpret_cast<uint32_t*>(w)[b] = 0u;
+            if (b == 0) atomicOr(status, GEAR_STATUS_NO_WEIGHT);
+            continue;
+        }
+        const uint64_t r = scale_draw(splitmix64_out(seed, 2 * (uint64_t)b), S);
+        int64_t lo = 0, hi = N;  // the smallest i with C_i > r lies in [lo, hi]
+        while (lo < hi) {
+            const int64_t mid = (lo + hi) >> 1;
+            if (C[small_pos(mid)] > r) hi = mid;
+            else lo = mid + 1;
+        }
+        const uint32_t pv = (uint32_t)(C[small_pos(lo)] - (lo > 0 ? C[small_pos(lo - 1)] : 0));
+        idx[b] = lo;
+        start[b] = (int32_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b + 1), span);
+        if (want_w) reinterpret_cast<uint32_t*>(w)[b] = pv;
+        m = pv < m ? pv : m;
+    }
+    if (!want_w) return;
+    if (global_min) m = pmin;
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+        const uint32_t o = __shfl_xor(m, d);
+        m = o < m ? o : m;
+    }
+    if (lane == 0) s_min[wave] = m;
+    __syncthreads();
+    m = s_min[0];
+    for (int q = 1; q < kSmallThreads / 64; q++) m = s_min[q] < m ? s_min[q] : m;
+    for (int64_t b = t; b < B; b += kSmallThreads) {
+        const uint32_t pb = reinterpret_cast<const uint32_t*>(w)[b];
+        w[b] = (pb == 0u || m == 0u) ? 0.0f : (float)pow((double)m / (double)pb, beta);
+    }
+}
+
 // FIFO / LIFO: ring arithmetic from the oldest / newest live position.
 // Uniform: r = floor(u * n / 2^64) over the n live trajectories.
 // A ring table's positions are its slots, and its live slots are [0, n).
@@ -390,6 +489,18 @@ hipError_t launch_is_weights(Table& t, int32_t B, float beta, int search_grid, f
     return hipGetLastError();
 }
 
+bool small_select_applies(const Table& t, int32_t B) {
+    return t.N <= kSmallN && B <= kSmallMaxB && !(t.options & GEAR_OPT_INCREMENTAL_TREE);
+}
+
+hipError_t launch_small_select(Table& t, int32_t B, int32_t L, uint64_t seed, float beta, int64_t* idx,
+                               int32_t* start, float* w, hipStream_t s) {
+    hipLaunchKernelGGL(small_select_kernel, dim3(1), dim3(kSmallThreads), 0, s, t.priority, t.N, B,
+                       (uint64_t)(t.T - L + 1), seed, w ? 1 : 0, (t.options & GEAR_OPT_IS_GLOBAL_MIN) ? 1 : 0,
+                       (double)beta, t.status, idx, start, w);
+    return hipGetLastError();
+}
+
 hipError_t launch_simple_select(Table& t, int32_t strategy, int32_t B, int32_t L, uint64_t seed, int64_t* idx,
                                 int32_t* start, float* w, hipStream_t s) {
     const int64_t live = live_count(t);
@@ -437,6 +548,11 @@ extern "C" int gear_select(gear_table* h, int32_t strategy, int32_t B, int32_t L
     if (strategy != GEAR_PRIORITIZED) {
         hipError_t e = gear::launch_simple_select(*t, strategy, B, L, seed, d_idx, d_start, d_weights, s);
         return e == hipSuccess ? GEAR_OK : hip_fail(e, "gear_select: launch");
+    }
+    if (gear::small_select_applies(*t, B)) {
+        // One launch; the sum tree is left as it is (still marked for a rescan if stale).
+        hipError_t e = gear::launch_small_select(*t, B, L, seed, beta, d_idx, d_start, d_weights, s);
+        return e == hipSuccess ? GEAR_OK : hip_fail(e, "gear_select: small-table launch");
     }
     if (t->cdf_dirty) {
         hipError_t e = gear::launch_scan(*t, s);

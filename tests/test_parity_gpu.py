@@ -496,3 +496,38 @@ def test_topk_threshold_at_exponent_boundaries():
             assert t.sync() == (0 if st == oracle.OK else gear.GEAR_STATUS_NO_WEIGHT)
     finally:
         t.close()
+
+
+@pytest.mark.parametrize("global_min", [False, True], ids=["batch-min", "global-min"])
+def test_small_table_one_launch_and_tree_paths_alternate(global_min):
+    """A table of at most 16384 slots selects in one launch for batches up
+    to 2048 and through the sum tree above that; alternating the two with
+    updates in between must give the oracle's draws and weights every time
+    (the tree is rescanned when it went stale during one-launch selects)."""
+    rng = np.random.default_rng(31)
+    N, T = 16384, 3
+    p = rng.integers(1, 1000, N).astype(np.uint32)
+    p[rng.random(N) < 0.1] = 0
+    t = gear.Table([2], capacity=N, T=T, residency=gear.GEAR_DEVICE, device=0)
+    try:
+        if global_min:
+            t.set_options(gear.GEAR_OPT_IS_GLOBAL_MIN)
+        t.insert([np.zeros((N, 2 * T), np.uint8)], p)
+        for it, B in enumerate([100, 3000, 2048, 2049, 1, 4096, 777]):
+            say("small table, B=%d, global_min=%s" % (B, global_min))
+            seed = 1000 + it
+            idx, start, wt = t.select(gear.GEAR_PRIORITIZED, B, 2, seed, 0.4, weights=True)
+            st, oidx, ostart, ow = oracle.select(oracle.PRIORITIZED, p, N, T, B, 2, seed, 0.4, True,
+                                                 global_min=global_min)
+            assert st == oracle.OK
+            np.testing.assert_array_equal(host(idx), oidx)
+            np.testing.assert_array_equal(host(start), ostart)
+            assert_weights(host(wt), ow)
+            upd = rng.integers(0, N, 600).astype(np.int64)
+            newp = rng.integers(0, 2000, 600).astype(np.uint32)
+            t.update_priorities(torch.from_numpy(upd).to(cuda()), torch.from_numpy(newp).to(cuda()))
+            oracle.update(p, upd, newp)
+        np.testing.assert_array_equal(t.priorities(), p)
+        assert t.sync() == 0
+    finally:
+        t.close()
