@@ -531,3 +531,49 @@ def test_small_table_one_launch_and_tree_paths_alternate(global_min):
         assert t.sync() == 0
     finally:
         t.close()
+
+
+# ---------------------------------------------------------------------------
+# Seeded random configurations: table shapes, element sizes (all three
+# element widths, narrow and wide windows), fills that wrap, strategies,
+# batch sizes on both sides of the one-launch select's limit, window
+# lengths and weights, each replayed against the oracle.
+# ---------------------------------------------------------------------------
+
+_KINDS = [(gen.BYTES, 1), (gen.DONE_U8, 1), (gen.INT_MOD, 4), (gen.NORMAL_F32, 4), (gen.UNIFORM_F32, 4),
+          (gen.NORMAL_BF16, 2)]
+_PRIOS = [U1000, BIG, gen.PrioDist(gen.PRIO_UNIFORM, 1, 3), gen.PrioDist(gen.PRIO_PARETO, 1.5, float(1 << 24)),
+          gen.PrioDist(gen.PRIO_LOGNORMAL, 6.931471805599453, 1.0, float(1 << 24))]
+
+
+def _random_workload(k):
+    rng = np.random.default_rng(1000 + k)
+    large = rng.random() < 0.35  # above the one-launch select's 16384 slots
+    N = int(rng.integers(16385, 60001)) if large else int(np.exp(rng.uniform(0, np.log(16384))))
+    T = int(rng.integers(1, 9 if large else 41))
+    cols = []
+    for c in range(int(rng.integers(0, 4))):
+        kind, size = _KINDS[int(rng.integers(0, len(_KINDS)))]
+        elems = int(rng.choice([1, 2, 3, 4, 8, 16, 17, 64, 96]))
+        param = 16 if kind == gen.INT_MOD else 0
+        cols.append(gen.Column("c%d" % c, kind, elems, param=param))
+    # Keep the table within a few MB so the CPU oracle stays quick.
+    while cols and N * T * sum(c.elem_bytes for c in cols) > (6 << 20):
+        cols.pop()
+    n_insert = int(rng.integers(1, 2 * N + 1))
+    live = min(n_insert, N)
+    strategies = tuple(int(s) for s in rng.permutation(5)[:int(rng.integers(1, 4))])
+    B = int(rng.choice([1, 7, 256, 2048, 2049, 3000]))
+    if any(s in (0, 1, 4) for s in strategies):
+        B = min(B, live)
+    L = int(rng.integers(1, T + 1))
+    return _custom("random-%d" % k, N, T, cols, n_insert, _PRIOS[int(rng.integers(0, len(_PRIOS)))], B, L,
+                   strategies=strategies, weights=bool(rng.integers(0, 2)), seed=int(rng.integers(1, 1 << 30)))
+
+
+RANDOM = [_random_workload(k) for k in range(24)]
+
+
+@pytest.mark.parametrize("w", RANDOM, ids=[w.name for w in RANDOM])
+def test_random_configurations(w):
+    _run_full(w, iterations=2)
