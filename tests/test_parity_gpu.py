@@ -571,7 +571,7 @@ def _random_workload(k):
                    strategies=strategies, weights=bool(rng.integers(0, 2)), seed=int(rng.integers(1, 1 << 30)))
 
 
-RANDOM = [_random_workload(k) for k in range(24)]
+RANDOM = [_random_workload(k) for k in range(64)]
 
 
 @pytest.mark.parametrize("w", RANDOM, ids=[w.name for w in RANDOM])
