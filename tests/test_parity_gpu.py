@@ -572,6 +572,10 @@ def _random_workload(k):
 
 
 RANDOM = [_random_workload(k) for k in range(64)]
+# The same kind of configurations with the table in pinned host memory,
+# read zero-copy by the gather.
+RANDOM += [dataclasses.replace(_random_workload(k), name="random-host-%d" % k, host_table=True)
+           for k in range(64, 80)]
 
 
 @pytest.mark.parametrize("w", RANDOM, ids=[w.name for w in RANDOM])
