@@ -64,7 +64,8 @@ def _run_full(w, iterations, strategies=None, check_contents=True, options=0):
                 say("%s iteration %d strategy %d" % (w.name, it, strat))
                 B = w.B
                 idx, start, wt = t.select(strat, B, w.L, seed, w.beta, weights=w.weights)
-                st, oidx, ostart, ow = s.select(strat, B, w.L, seed, w.beta, weights=w.weights)
+                st, oidx, ostart, ow = s.select(strat, B, w.L, seed, w.beta, weights=w.weights,
+                                                global_min=bool(options & gear.GEAR_OPT_IS_GLOBAL_MIN))
                 assert st == oracle.OK
                 np.testing.assert_array_equal(host(idx), oidx)
                 np.testing.assert_array_equal(host(start), ostart)
@@ -581,3 +582,14 @@ RANDOM += [dataclasses.replace(_random_workload(k), name="random-host-%d" % k, h
 @pytest.mark.parametrize("w", RANDOM, ids=[w.name for w in RANDOM])
 def test_random_configurations(w):
     _run_full(w, iterations=2)
+
+
+RANDOM_OPT = [(_random_workload(k), gear.GEAR_OPT_INCREMENTAL_TREE) for k in range(80, 96)]
+RANDOM_OPT += [(_random_workload(k), gear.GEAR_OPT_IS_GLOBAL_MIN) for k in range(96, 112)]
+RANDOM_OPT += [(_random_workload(k), gear.GEAR_OPT_INCREMENTAL_TREE | gear.GEAR_OPT_IS_GLOBAL_MIN)
+               for k in range(112, 120)]
+
+
+@pytest.mark.parametrize("w,options", RANDOM_OPT, ids=["%s-opt%d" % (w.name, o) for w, o in RANDOM_OPT])
+def test_random_configurations_with_options(w, options):
+    _run_full(w, iterations=3, options=options)
