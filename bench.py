@@ -571,7 +571,7 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (requested %d GPUs, WORLD_SIZE=%d)"
+        print("bench.py measures one GPU: there is no multi-GPU path here (requested %d GPUs, WORLD_SIZE=%d)"
               % (args.gpus, world), file=sys.stderr)
         sys.exit(2)
     if args.calibrate:
