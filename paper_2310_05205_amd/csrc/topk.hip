@@ -100,6 +100,17 @@ constexpr int64_t kBatch = (int64_t)kVec * kTopkThreads * 4;
 
 __device__ __forceinline__ void load_batch(const uint32_t* __restrict__ prio, int64_t base, int64_t hi,
                                            uint32_t v[kVec][4]) {
+    if (base + kBatch <= hi) {
+        // The whole batch is in range (every batch but a ragged last one):
+        // a branch the workgroup takes as one, so the loads are issued
+        // back to back, none waiting for another.
+#pragma unroll
+        for (int k = 0; k < kVec; k++) {
+            const uint4 x = *reinterpret_cast<const uint4*>(prio + base + ((int64_t)k * kTopkThreads + threadIdx.x) * 4);
+            v[k][0] = x.x; v[k][1] = x.y; v[k][2] = x.z; v[k][3] = x.w;
+        }
+        return;
+    }
 #pragma unroll
     for (int k = 0; k < kVec; k++) {
         const int64_t e = base + ((int64_t)k * kTopkThreads + threadIdx.x) * 4;
