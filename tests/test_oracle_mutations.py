@@ -48,6 +48,10 @@ MUTATIONS = [
     ("LIFO over the commit list in FIFO order", "order[n - 1 - b]", "order[b]"),
     ("uniform over capacity", "oracle_draw(seed, 2u * (uint64_t)b), (uint64_t)n);",
      "oracle_draw(seed, 2u * (uint64_t)b), (uint64_t)N);"),
+    ("uniform index on the start's counter", "oracle_draw(seed, 2u * (uint64_t)b), (uint64_t)n);",
+     "oracle_draw(seed, 2u * (uint64_t)b + 1u), (uint64_t)n);"),
+    ("uniform index on counter b", "oracle_draw(seed, 2u * (uint64_t)b), (uint64_t)n);",
+     "oracle_draw(seed, (uint64_t)b), (uint64_t)n);"),
     ("uniform ignores the commit list", "idx[b] = order != NULL ? order[r] : r;", "idx[b] = r;"),
     # window starts
     ("start reuses the index draw", "start[b] = (int32_t)oracle_bounded(oracle_draw(seed, 2u * (uint64_t)b + 1u),\n"

@@ -194,6 +194,66 @@ def test_uniform_ranges_and_partial_fill():
     assert np.all(start == 0)
 
 
+def _splitmix64_python(seed, c):
+    """Output c of splitmix64 seeded with `seed`, in Python integers from the
+    generator's published definition (state advanced by the golden gamma c+1
+    times, then the two xor-shift-multiply rounds and a final xor-shift)."""
+    m = (1 << 64) - 1
+    z = (seed + (c + 1) * 0x9E3779B97F4A7C15) & m
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & m
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & m
+    return z ^ (z >> 31)
+
+
+def test_python_splitmix64_agrees_with_published_outputs():
+    # Vigna's splitmix64.c from state 0; the same words as the oracle's pin.
+    assert [_splitmix64_python(0, c) for c in range(3)] == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4,
+                                                            0x06C45D188009454F]
+
+
+@pytest.mark.parametrize("N,n_insert,seed", [(1000, 300, 77), (1000, 1000, 5), (64, 1000, 123456789),
+                                             (1, 9, 3), (7, 7 + 3, (1 << 64) - 1)])
+def test_uniform_index_draw_matches_definition(N, n_insert, seed):
+    # Uniform over the n live slots: idx_b = floor(u_2b * n / 2^64), with u_c
+    # output c of the stream (index draw on the even counter, window start on
+    # the odd one).  Ring tables: partly filled (n < N) and wrapped (n = N).
+    T, L, B = 12, 5, 2000
+    store = _stamped_store(N, T, n_insert)
+    n = min(n_insert, N)
+    st, idx, start, w = store.select(oracle.UNIFORM, B, L, seed, weights=True)
+    assert st == oracle.OK
+    expect_idx = [(_splitmix64_python(seed, 2 * b) * n) >> 64 for b in range(B)]
+    expect_start = [(_splitmix64_python(seed, 2 * b + 1) * (T - L + 1)) >> 64 for b in range(B)]
+    np.testing.assert_array_equal(idx, np.array(expect_idx, dtype=np.int64))
+    np.testing.assert_array_equal(start, np.array(expect_start, dtype=np.int32))
+    assert np.all(w == 1.0)
+
+
+@pytest.mark.parametrize("removal", [oracle.FIFO, oracle.LIFO])
+def test_uniform_index_draw_on_a_commit_list(removal):
+    # With an index manager the r-th draw picks the r-th oldest committed
+    # index: idx_b = order[floor(u_2b * n / 2^64)], n the committed count.
+    N, T, L, B, seed = 50, 6, 2, 1500, 4242
+    m = oracle.IndexManager(N, removal, 40)
+    prio = np.zeros(N, dtype=np.uint32)
+    rng = np.random.default_rng(removal)
+    committed = []                               # the commit order, kept by this test
+    for step in range(12):
+        st, got = m.allocate(int(rng.integers(1, 9)), prio)
+        assert st == oracle.OK
+        victims = [i for i in committed if prio[i] == 0]
+        committed = [i for i in committed if i not in victims]
+        order = list(rng.permutation(got))
+        assert m.commit(order, np.full(len(order), 3, dtype=np.uint32), prio) == oracle.OK
+        committed += [int(i) for i in order]
+    np.testing.assert_array_equal(m.order(), committed)
+    n = len(committed)
+    st, idx, start, _ = oracle.select(oracle.UNIFORM, prio, 0, T, B, L, seed, order=m.order())
+    assert st == oracle.OK
+    expect = [committed[(_splitmix64_python(seed, 2 * b) * n) >> 64] for b in range(B)]
+    np.testing.assert_array_equal(idx, np.array(expect, dtype=np.int64))
+
+
 def test_window_start_matches_definition():
     p = np.ones(10, dtype=np.uint32)
     T, L, B, seed = 1000, 20, 300, 31337
