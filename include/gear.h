@@ -35,8 +35,8 @@
  *   - A table is not thread-safe.  All calls on one table must be ordered:
  *     issue them from one host thread, on one stream, or order the streams
  *     with events.  Separate tables are independent.
- *   - HIP graph capture: gear_collect keeps no host-side state and may be
- *     captured and replayed.  Selection, insertion, allocation, commits and
+ *   - HIP graph capture: gear_collect and gear_select_prioritized_noalloc
+ *     keep no host-side state and may be captured and replayed.  Selection, insertion, allocation, commits and
  *     updates read and change host-side state when they are called (ring
  *     counters, whether the sum tree is current, which copy of its upper
  *     levels is live), so a replayed capture would repeat stale decisions:
@@ -92,6 +92,8 @@ extern "C" {
 #define GEAR_MAX_COLUMNS   64
 #define GEAR_MAX_BATCH     (1 << 24)
 #define GEAR_MAX_TOPK      16384        /* B limit of GEAR_TOPK */
+#define GEAR_NOALLOC_MAX_N (1 << 24)    /* N limit of gear_select_prioritized_noalloc */
+#define GEAR_NOALLOC_SCRATCH_BYTES 536832  /* its fixed device scratch per GPU */
 
 typedef struct gear_table gear_table;
 
@@ -363,6 +365,35 @@ int gear_is_weights(gear_table *t, const uint32_t *d_sel_prio, int32_t B, float 
 int gear_topk_merge(const uint32_t *d_prio, const int64_t *d_gidx, int32_t G, int32_t K, int32_t T, int32_t L,
                     uint64_t seed, int64_t *d_idx, int32_t *d_start, float *d_weights, uint32_t *d_out_prio,
                     void *stream);
+
+/*
+ * gear_select_prioritized_noalloc - gear_select(GEAR_PRIORITIZED) over a
+ * caller's priority array, allocating nothing.  For callers that cannot
+ * allocate device memory: code being captured into a HIP graph, serving
+ * loops that forbid allocation.  It keeps no host-side state besides the
+ * scratch address, so a captured call replays correctly with the array's
+ * contents at replay time.  Runs on the current HIP device.
+ *
+ *   d_priority  device uint32[N]: slot i is drawn with probability p_i / S,
+ *               S the sum; zero is never drawn
+ *   N           1 .. GEAR_NOALLOC_MAX_N (all N slots are live)
+ *   T, L, B, seed, beta, d_idx, d_start, d_weights
+ *               as for gear_select: the same draws, windows and weights a
+ *               table holding these priorities returns
+ *
+ * Scratch: the sum tree (GEAR_NOALLOC_SCRATCH_BYTES in all, sized for
+ * GEAR_NOALLOC_MAX_N) lives in a fixed device array of the library, one per
+ * GPU, held until the process ends.  Every call on a GPU shares it, so calls
+ * that overlap on one GPU (different streams, or different host threads,
+ * without ordering) race and give wrong draws; order them.  When every
+ * priority is zero, each draw gets idx = -1, start = 0, weight 0 (there is
+ * no status word to read).
+ * Errors: GEAR_E_INVAL (NULL pointer, N above GEAR_NOALLOC_MAX_N, B, L or T
+ * out of range, NaN beta; nothing enqueued), GEAR_E_HIP.
+ */
+int gear_select_prioritized_noalloc(const uint32_t *d_priority, int64_t N, int32_t T, int32_t B, int32_t L,
+                                    uint64_t seed, float beta, int64_t *d_idx, int32_t *d_start,
+                                    float *d_weights, void *stream);
 
 /*
  * gear_update_priorities - write new priorities for selected slots (Sec. 3.2:

@@ -30,6 +30,8 @@
 // C, and computes the IS weights, all in one launch.
 //
 // FIFO, LIFO and uniform selection are one thread per draw.
+#include <mutex>
+
 #include "gear_internal.h"
 #include "wave.h"
 
@@ -569,4 +571,130 @@ extern "C" int gear_select(gear_table* h, int32_t strategy, int32_t B, int32_t L
         if (e != hipSuccess) return hip_fail(e, "gear_select: weight launch");
     }
     return GEAR_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Prioritized selection without allocation: the kernels above, run over a
+// caller's priority array with the sum tree, the per-workgroup minima and
+// the status word in a fixed file-scope device array instead of table
+// memory.  For callers that cannot allocate (graph capture, serving loops).
+// ---------------------------------------------------------------------------
+namespace gear {
+namespace {
+
+constexpr int64_t kNaTiles = GEAR_NOALLOC_MAX_N / kTile;            // level 0 entries
+constexpr int64_t kNaLevel1 = (kNaTiles + kFanout - 1) / kFanout;     // level 1 entries (the top)
+static_assert(kNaLevel1 <= kFanout, "two levels cover every allowed table");
+static_assert(GEAR_NOALLOC_MAX_N % (kTile * kTilesPerChunk) == 0, "whole scan chunks");
+// Layout in 64-bit words: tile sums | level 1 (the scan adds into it) |
+// level 1 spare (the scan's zeroing target, never read) | wg_min (uint32) |
+// status (uint32).
+constexpr int64_t kNaOffTiles = 0;
+constexpr int64_t kNaOffLevel1 = kNaOffTiles + kNaTiles;
+constexpr int64_t kNaOffSpare = kNaOffLevel1 + kFanout;
+constexpr int64_t kNaOffMin = kNaOffSpare + kFanout;
+constexpr int64_t kNaOffStatus = kNaOffMin + kSearchMaxGrid / 2;
+constexpr int64_t kNaWords = (kNaOffStatus + 1 + 31) / 32 * 32;
+static_assert(kNaWords * 8 == GEAR_NOALLOC_SCRATCH_BYTES, "header states the scratch size");
+
+// Holds every call's scratch on each device, until the process ends.
+static __device__ __align__(256) uint64_t scratch[kNaWords];
+
+// Device address of `scratch` on each device, looked up once per device
+// with that device current (host code must not pass the symbol itself).
+constexpr int kNaMaxDevices = 64;
+std::mutex g_na_mutex;
+uint64_t* g_na_ptr[kNaMaxDevices] = {};
+
+// Zeroes the level-1 nodes the scan accumulates into and the status word:
+// a kernel, not a memset, so that a captured graph replays it faithfully.
+__global__ void noalloc_clear_kernel(uint64_t* __restrict__ level1, uint32_t* __restrict__ status) {
+    const int k = threadIdx.x;
+    if (k < kFanout) level1[k] = 0;
+    if (k == 0) *status = 0u;
+}
+
+hipError_t noalloc_scratch(int dev, uint64_t** out) {
+    std::lock_guard<std::mutex> lock(g_na_mutex);
+    if (g_na_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_na_ptr[dev] = static_cast<uint64_t*>(p);
+    }
+    *out = g_na_ptr[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+}  // namespace gear
+
+extern "C" int gear_select_prioritized_noalloc(const uint32_t* d_priority, int64_t N, int32_t T, int32_t B,
+                                               int32_t L, uint64_t seed, float beta, int64_t* d_idx,
+                                               int32_t* d_start, float* d_weights, void* stream) {
+    using namespace gear;
+    if (d_priority == nullptr || d_idx == nullptr || d_start == nullptr)
+        return fail(GEAR_E_INVAL, "gear_select_prioritized_noalloc: NULL pointer argument");
+    if (N < 1 || N > GEAR_NOALLOC_MAX_N)
+        return fail(GEAR_E_INVAL, "gear_select_prioritized_noalloc: N must lie in [1, GEAR_NOALLOC_MAX_N]");
+    if (B < 1 || B > GEAR_MAX_BATCH) return fail(GEAR_E_INVAL, "gear_select_prioritized_noalloc: B out of range");
+    if (T < 1 || L < 1 || L > T) return fail(GEAR_E_INVAL, "gear_select_prioritized_noalloc: L must lie in [1, T]");
+    if (!(beta == beta)) return fail(GEAR_E_INVAL, "gear_select_prioritized_noalloc: beta is NaN");
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "gear_select_prioritized_noalloc: hipGetDevice");
+    if (dev < 0 || dev >= kNaMaxDevices) return fail(GEAR_E_INVAL, "gear_select_prioritized_noalloc: device ordinal above 63");
+    uint64_t* base = nullptr;
+    e = noalloc_scratch(dev, &base);
+    if (e != hipSuccess) return hip_fail(e, "gear_select_prioritized_noalloc: hipGetSymbolAddress");
+    uint32_t* status = reinterpret_cast<uint32_t*>(base + kNaOffStatus);
+    uint32_t* wg_min = reinterpret_cast<uint32_t*>(base + kNaOffMin);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const uint64_t span = (uint64_t)(T - L + 1);
+
+    if (N <= kSmallN && B <= kSmallMaxB) {
+        // One launch, as gear_select takes for a table this small.
+        hipLaunchKernelGGL(small_select_kernel, dim3(1), dim3(kSmallThreads), 0, s, d_priority, N, B, span, seed,
+                           d_weights ? 1 : 0, 0, (double)beta, status, d_idx, d_start, d_weights);
+        e = hipGetLastError();
+        return e == hipSuccess ? GEAR_OK : hip_fail(e, "gear_select_prioritized_noalloc: small-table launch");
+    }
+    const int64_t ntiles = (N + kTile - 1) / kTile;
+    const int64_t nchunks = (ntiles + kTilesPerChunk - 1) / kTilesPerChunk;
+    Levels lv{}, upper{}, spare{};
+    lv.nlevels = ntiles > kFanout ? 2 : 1;
+    lv.level[0] = base + kNaOffTiles;
+    lv.size[0] = ntiles;
+    upper.nlevels = spare.nlevels = lv.nlevels;
+    if (lv.nlevels == 2) {
+        lv.level[1] = upper.level[1] = base + kNaOffLevel1;
+        spare.level[1] = base + kNaOffSpare;
+        lv.size[1] = upper.size[1] = spare.size[1] = (ntiles + kFanout - 1) / kFanout;
+    }
+    const char* what = "gear_select_prioritized_noalloc: clear launch";
+    hipLaunchKernelGGL(noalloc_clear_kernel, dim3(1), dim3(kFanout), 0, s, base + kNaOffLevel1, status);
+    if ((e = hipGetLastError()) == hipSuccess) {
+        what = "gear_select_prioritized_noalloc: scan launch";
+        hipLaunchKernelGGL(scan_kernel<false>, dim3((unsigned)nchunks), dim3(256), 0, s, d_priority, N, upper, spare,
+                           lv.level[0], ntiles, static_cast<uint32_t*>(nullptr));
+        e = hipGetLastError();
+    }
+    const int64_t gw = ((int64_t)B + 3) / 4;
+    const int grid = (int)(gw < kSearchMaxGrid ? gw : kSearchMaxGrid);
+    if (e == hipSuccess) {
+        what = "gear_select_prioritized_noalloc: search launch";
+        Shard sh{};
+        sh.G = 1;
+        hipLaunchKernelGGL(search_kernel<false>, dim3(grid), dim3(256), 0, s, d_priority, N, lv, B, span, seed,
+                           d_weights ? 1 : 0, sh, wg_min, status, d_idx, d_start,
+                           reinterpret_cast<uint32_t*>(d_weights));
+        e = hipGetLastError();
+    }
+    if (e == hipSuccess && d_weights) {
+        what = "gear_select_prioritized_noalloc: weight launch";
+        hipLaunchKernelGGL(is_weights_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s, B, (double)beta,
+                           static_cast<const uint32_t*>(wg_min), grid, d_weights);
+        e = hipGetLastError();
+    }
+    return e == hipSuccess ? GEAR_OK : hip_fail(e, what);
 }

@@ -34,6 +34,8 @@ GEAR_MAX_CAPACITY = 1 << 30
 GEAR_MAX_COLUMNS = 64
 GEAR_MAX_BATCH = 1 << 24
 GEAR_MAX_TOPK = 16384
+GEAR_NOALLOC_MAX_N = 1 << 24
+GEAR_NOALLOC_SCRATCH_BYTES = 536832
 GEAR_OPT_INCREMENTAL_TREE = 1
 GEAR_OPT_IS_GLOBAL_MIN = 2
 
@@ -77,11 +79,13 @@ def lib():
         L.gear_select_shard.argtypes = [vp, i32, i32, vp, i64, i32, i32, u64, vp, vp, vp, vp]
         L.gear_is_weights.argtypes = [vp, vp, i32, ctypes.c_float, vp, vp]
         L.gear_topk_merge.argtypes = [vp, vp, i32, i32, i32, i32, u64, vp, vp, vp, vp, vp]
+        L.gear_select_prioritized_noalloc.argtypes = [vp, i64, i32, i32, i32, u64, ctypes.c_float, vp, vp, vp, vp]
         for name in ["gear_table_create", "gear_table_destroy", "gear_insert", "gear_select", "gear_collect",
                      "gear_update_priorities", "gear_table_sync", "gear_table_info", "gear_table_column",
                      "gear_table_priorities", "gear_table_set_options", "gear_table_use_allocator",
                      "gear_allocate", "gear_commit", "gear_allocator_info", "gear_write_rows", "gear_shard_total",
-                     "gear_select_shard", "gear_is_weights", "gear_topk_merge"]:
+                     "gear_select_shard", "gear_is_weights", "gear_topk_merge",
+                     "gear_select_prioritized_noalloc"]:
             getattr(L, name).restype = ctypes.c_int
         L.gear_last_error.argtypes = []
         L.gear_last_error.restype = ctypes.c_char_p
@@ -127,6 +131,12 @@ def gear_insert(table, n, col_src, priorities, stream=0):
 def gear_select(table, strategy, B, L, seed, beta, d_idx, d_start, d_weights=0, stream=0):
     _check(lib().gear_select(table, int(strategy), int(B), int(L), int(seed) & ((1 << 64) - 1),
                              ctypes.c_float(beta), d_idx, d_start, d_weights or None, stream))
+
+
+def gear_select_prioritized_noalloc(d_priority, N, T, B, L, seed, beta, d_idx, d_start, d_weights=0, stream=0):
+    _check(lib().gear_select_prioritized_noalloc(d_priority, int(N), int(T), int(B), int(L),
+                                                 int(seed) & ((1 << 64) - 1), ctypes.c_float(beta), d_idx, d_start,
+                                                 d_weights or None, stream))
 
 
 def gear_collect(table, d_idx, d_start, B, L, col_ids, d_out, stream=0):

@@ -71,6 +71,11 @@ def test_argument_validation_without_device():
     assert lib.gear_is_weights(None, None, 1, ctypes.c_float(0), None, None) == gear.GEAR_E_INVAL
     assert lib.gear_topk_merge(None, None, 0, 1, 1, 1, 0, None, None, None, None, None) == gear.GEAR_E_INVAL
     assert lib.gear_topk_merge(None, None, 2, 1, 1, 1, 0, None, None, None, None, None) == gear.GEAR_E_INVAL
+    f0 = ctypes.c_float(0)
+    assert lib.gear_select_prioritized_noalloc(None, 16, 4, 4, 1, 0, f0, None, None, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_select_prioritized_noalloc(16, gear.GEAR_NOALLOC_MAX_N + 1, 4, 4, 1, 0, f0, 16, 16, None,
+                                               None) == gear.GEAR_E_INVAL
+    assert "GEAR_NOALLOC_MAX_N" in gear.gear_last_error()
     with pytest.raises(gear.GearError) as e:
         gear.gear_table_create([4], 16, 0)
     assert e.value.code == gear.GEAR_E_INVAL
