@@ -50,6 +50,7 @@ class HipEvents:
         h.hipEventRecord.argtypes = [vp, vp]
         h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), vp, vp]
         h.hipEventDestroy.argtypes = [vp]
+        h.hipStreamWaitEvent.argtypes = [vp, vp, ctypes.c_uint]
         self.h = h
         self.made = []
 
@@ -65,6 +66,10 @@ class HipEvents:
 
     def record(self, e, stream_handle):
         self._ok(self.h.hipEventRecord(e, ctypes.c_void_p(stream_handle)), "hipEventRecord")
+
+    def wait(self, stream_handle, e):
+        """Work enqueued on the stream after this waits for event e."""
+        self._ok(self.h.hipStreamWaitEvent(ctypes.c_void_p(stream_handle), e, 0), "hipStreamWaitEvent")
 
     def elapsed_ms(self, a, b):
         ms = ctypes.c_float()
@@ -86,6 +91,12 @@ def parse():
                     choices=["mat", "gato-host", "dt", "dt-full", "tiny", "select-stress", "topk", "mat-insert",
                              "shard-select"])
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
+    ap.add_argument("--serial", action="store_true",
+                    help="issue every step in order on one stream (default: select/update overlap the gather)")
+    ap.add_argument("--group", type=int, default=2,
+                    help="steps per cross-stream handshake when select/update overlap the gather")
+    ap.add_argument("--legs", default="all", choices=["all", "headline"],
+                    help="default MAT run: also measure the host-link, whole-trajectory and selection legs")
     ap.add_argument("--incremental", action="store_true",
                     help="keep the selection sum tree current across updates (no rescan per step)")
     ap.add_argument("--global-min", action="store_true",
@@ -312,9 +323,10 @@ def cpu_baseline(w, target_s, global_min=False):
 
     import gen
     import oracle
-    from tests.helpers import oracle_priorities
 
-    p, next_seq = oracle_priorities(w)
+    ring = oracle.Store([], w.N, w.T)      # the priority array after all of w's insertions
+    ring.insert([], gen.insert_priorities(w.prio, w.seed, 0, w.n_insert))
+    p, next_seq = ring.priority, ring.next_seq
     seed = gen.select_seed(w.seed, 0)
     strat = w.strategies[0]
     updates = strat in (oracle.PRIORITIZED, oracle.TOPK)  # as in the GPU step
@@ -567,6 +579,279 @@ def run_shard(args):
     print(json.dumps(line), flush=True)
 
 
+class Step:
+    """One workload's step on a table, issued through the C ABI with its
+    arguments built once: select into buffer set k, collect from set k into
+    batch set k, update the priorities of set k's draws.  The sets (indices,
+    starts, weights and one batch buffer per column) are used in turn, so
+    no batch line is still cached from the step before."""
+
+    def __init__(self, t, w, nsets, iters, dev):
+        import numpy as np
+        import torch
+
+        import gen
+        from paper_2310_05205_amd import gear
+
+        self.gear, self.lib = gear, gear.lib()
+        self.tab = ctypes.c_void_p(t.handle)
+        self.B, self.L = w.B, w.L
+        self.strategy = w.strategies[0]
+        self.updates = self.strategy in (gear.GEAR_PRIORITIZED, gear.GEAR_TOPK)
+        self.weights = bool(w.weights)
+        self.beta = ctypes.c_float(w.beta)
+        self.ncols = len(w.elem_bytes)
+        B, L = w.B, w.L
+        self.idx = [torch.empty(B, dtype=torch.int64, device=dev) for _ in range(nsets)]
+        self.start = [torch.empty(B, dtype=torch.int32, device=dev) for _ in range(nsets)]
+        self.wts = [torch.empty(B, dtype=torch.float32, device=dev) for _ in range(nsets)]
+        self.outs = [[torch.empty(B * L * e, dtype=torch.uint8, device=dev) for e in w.elem_bytes]
+                     for _ in range(nsets)]
+        vp = lambda x: ctypes.c_void_p(x.data_ptr())
+        self.ip = [vp(x) for x in self.idx]
+        self.sp = [vp(x) for x in self.start]
+        self.wp = [vp(x) if self.weights else None for x in self.wts]
+        self.op = [gear._ptr_array([o.data_ptr() for o in outs]) for outs in self.outs]
+        self.seeds = [ctypes.c_uint64(gen.select_seed(w.seed, it)) for it in range(iters)]
+        if self.updates:
+            self.newp = torch.from_numpy(np.stack([gen.update_priorities(w.prio, w.seed, it, B)
+                                                   for it in range(iters)])).to(dev)
+            self.np_ = [vp(self.newp[it]) for it in range(iters)]
+
+    def _ok(self, rc, what):
+        if rc != 0:
+            raise RuntimeError("%s failed: %s" % (what, self.gear.gear_last_error()))
+
+    def select(self, it, k, sh):
+        self._ok(self.lib.gear_select(self.tab, self.strategy, self.B, self.L, self.seeds[it], self.beta, self.ip[k],
+                                      self.sp[k], self.wp[k], sh), "gear_select")
+
+    def collect(self, k, sh):
+        self._ok(self.lib.gear_collect(self.tab, self.ip[k], self.sp[k], self.B, self.L, None, self.ncols, self.op[k],
+                                       sh), "gear_collect")
+
+    def update(self, it, k, sh):
+        self._ok(self.lib.gear_update_priorities(self.tab, self.ip[k], self.np_[it], self.B, sh),
+                 "gear_update_priorities")
+
+
+def run_steps(t, w, K, W, dev, pipelined, group=2, stage_steps=50, serial_too=False):
+    """W untimed steps, then K timed ones, of workload w on table t.
+
+    Serial: select, collect and update of each step on one stream, in turn
+    over two buffer sets.
+    Pipelined: select and update on a second stream S, collect on the
+    current stream C, in groups of `group` steps over 2*group buffer sets.
+    S issues the selects and updates of a group, then one event; C waits for
+    that event once and runs the group's gathers, then records one event,
+    which S waits for before it reuses those buffer sets two groups later.
+    Every select still follows the previous step's update on S, so each step
+    draws exactly what the serial order draws; the selects and updates of
+    the next group overlap this group's gathers.  A cross-stream wait and a
+    marker between two gathers cost about 6 us (measured on gfx950 with
+    64 MB copies), which the groups pay once per group instead of per step.
+
+    Returns wall time, the mean gather launch time in the timed region, a
+    per-stage breakdown from a one-stream loop after the timed region, and,
+    with serial_too, the serial step time.  Gather launches are timed with
+    HIP events on C: serially, an event before and after each gather;
+    pipelined, an event after C's wait and the group's closing event, which
+    bracket the group's gathers and nothing else."""
+    import numpy as np
+    import torch
+
+    nsets = 2 * group if pipelined else 2
+    step = Step(t, w, nsets, W + K, dev)
+    hev = HipEvents()
+    C = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    side = torch.cuda.Stream(dev) if pipelined else None   # default priority, like every stream here
+    S = ctypes.c_void_p(side.cuda_stream) if pipelined else C
+    ngroups = (max(K, W) + group - 1) // group
+    sel_done = [hev.create() for _ in range(ngroups)]
+    col_begin = [hev.create() for _ in range(ngroups)]
+    col_done = [hev.create() for _ in range(ngroups)]
+    ev = [(hev.create(), hev.create()) for _ in range(K)]
+
+    def loop_serial(its, timed):
+        for j, it in enumerate(its):
+            k = j % nsets
+            step.select(it, k, C)
+            if timed:
+                hev.record(ev[j][0], C.value)
+            if step.ncols:
+                step.collect(k, C)
+            if timed:
+                hev.record(ev[j][1], C.value)
+            if step.updates:
+                step.update(it, k, C)
+
+    def loop_pipe(its):
+        its = list(its)
+        for g in range(0, (len(its) + group - 1) // group):
+            js = range(g * group, min(len(its), (g + 1) * group))
+            if g >= 2:
+                hev.wait(S.value, col_done[g - 2])
+            for j in js:
+                step.select(its[j], j % nsets, S)
+                if step.updates:
+                    step.update(its[j], j % nsets, S)
+            hev.record(sel_done[g], S.value)
+            hev.wait(C.value, sel_done[g])
+            hev.record(col_begin[g], C.value)
+            for j in js:
+                step.collect(j % nsets, C)
+            hev.record(col_done[g], C.value)
+        return (len(its) + group - 1) // group
+
+    if pipelined:
+        loop_pipe(range(W))
+    else:
+        loop_serial(range(W), False)
+    torch.cuda.synchronize()
+    if t.sync() != 0:
+        raise SystemExit("device status set during warm-up")
+    t0 = time.perf_counter()
+    ng = loop_pipe(range(W, W + K)) if pipelined else loop_serial(range(W, W + K), True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    status = t.sync()
+    if status != 0:
+        raise SystemExit("device status %d set during the timed steps" % status)
+    if pipelined:
+        col_ms = sum(hev.elapsed_ms(col_begin[g], col_done[g]) for g in range(ng)) / K
+    else:
+        col_ms = float(np.mean([hev.elapsed_ms(a, b) for a, b in ev]))
+    res = {"wall_s": wall, "collect_ms": col_ms, "step": step, "buffer_sets": nsets}
+    if serial_too:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        loop_serial(range(W, W + K), False)
+        torch.cuda.synchronize()
+        res["serial_ms_per_step"] = (time.perf_counter() - t0) * 1e3 / K
+
+    # Stage breakdown: one stream, events around every stage.
+    nb = min(K, stage_steps)
+    sev = [[hev.create() for _ in range(4)] for _ in range(nb)]
+    for j in range(nb):
+        it, k, e = W + j, j % nsets, sev[j]
+        hev.record(e[0], C.value)
+        step.select(it, k, C)
+        hev.record(e[1], C.value)
+        if step.ncols:
+            step.collect(k, C)
+        hev.record(e[2], C.value)
+        if step.updates:
+            step.update(it, k, C)
+        hev.record(e[3], C.value)
+    torch.cuda.synchronize()
+    if t.sync() != 0:
+        raise SystemExit("device status set during the stage loop")
+    stages = {"select": [hev.elapsed_ms(e[0], e[1]) for e in sev],
+              "collect": [hev.elapsed_ms(e[1], e[2]) for e in sev],
+              "update": [hev.elapsed_ms(e[2], e[3]) for e in sev]}
+    res["stages_mean"] = {k: float(np.mean(v)) for k, v in stages.items()}
+    res["stages_pct"] = {k: [round(float(x), 5) for x in np.percentile(v, [10, 50, 90])] for k, v in stages.items()
+                         if (k != "update" or step.updates) and (k != "collect" or step.ncols)}
+    hev.close()
+    return res
+
+
+def gather_roofline(w, col_ms, workload_key):
+    """Roofline object of the gather: algorithmic bytes per launch over the
+    mean event-timed launch duration."""
+    batch_bytes = w.B * w.L * sum(w.elem_bytes)
+    if w.host_table:
+        alg, peak, bound = batch_bytes, HOST_LINK_PEAK_GBS, "host-link"   # bytes crossing the link
+    else:
+        alg, peak, bound = 2 * batch_bytes, HBM_PEAK_GBS, "hbm"            # window bytes read + batch written
+    achieved = alg / (col_ms * 1e-3) / 1e9
+    return {"bound": bound, "achieved": round(achieved, 1), "peak": peak, "unit": "GB/s",
+            "frac": round(achieved / peak, 4), "traffic": profiled_traffic("collect_kernel", workload_key),
+            "kernel": "collect_kernel", "algorithmic_bytes_per_launch": alg, "avg_launch_ms": round(col_ms, 5)}
+
+
+def make_table(w, dev_index=0):
+    from gen.fill import fill_table
+    from paper_2310_05205_amd import gear
+    t = gear.Table(w.elem_bytes, w.N, w.T, gear.GEAR_HOST_PINNED if w.host_table else gear.GEAR_DEVICE, dev_index)
+    fill_table(w, lambda n, ptrs, prio: t.insert(ptrs, prio), device=dev_index)
+    return t
+
+
+def host_link_leg(dev, steps=10, warmup=2):
+    """Gato-like table (31.5 GB) in pinned host memory, read zero-copy:
+    prioritized select, gather of 1024 windows of 64 steps (805.8 MB over
+    the host link), update."""
+    from gen import configs
+    w = configs.GATO_HOST
+    t0 = time.perf_counter()
+    t = make_table(w)
+    setup = time.perf_counter() - t0
+    try:
+        r = run_steps(t, w, steps, warmup, dev, pipelined=False, stage_steps=steps)
+        roof = gather_roofline(w, r["collect_ms"], "gato-host")
+        st = r["step"]
+        link = host_link_extras(t, w, st.idx[0], st.start[0], st.outs[0], dev)
+        if not link["cpu_staged"]["matches_zero_copy"]:
+            raise SystemExit("the CPU-staged batch differs from the zero-copy batch")
+    finally:
+        t.close()
+    return {"workload": w.name, "residency": "pinned-host", "achieved_gbs": roof["achieved"],
+            "peak_gbs": HOST_LINK_PEAK_GBS, "frac": roof["frac"], "gate": 0.70,
+            "link_h2d_copy_gbs": link["link_h2d_copy_gbs"],
+            "frac_of_h2d_copy": round(roof["achieved"] / link["link_h2d_copy_gbs"], 4),
+            "avg_launch_ms": roof["avg_launch_ms"], "link_bytes_per_launch": roof["algorithmic_bytes_per_launch"],
+            "traffic": roof["traffic"], "steps": steps, "ms_per_step": round(r["wall_s"] * 1e3 / steps, 4),
+            "cpu_staged": link["cpu_staged"], "table_setup_s": round(setup, 1)}
+
+
+def dt_full_leg(dev, steps=50, warmup=5):
+    """DT-shaped table (6.55 GB, HBM), uniform selection of 512 whole
+    trajectories (L = T = 1000): 51.2 MB read and written per gather."""
+    from gen import configs
+    w = configs.DT_FULL
+    t = make_table(w)
+    try:
+        r = run_steps(t, w, steps, warmup, dev, pipelined=False, stage_steps=steps)
+    finally:
+        t.close()
+    roof = gather_roofline(w, r["collect_ms"], "dt-full")
+    return {"workload": w.name, "achieved_gbs": roof["achieved"], "peak_gbs": HBM_PEAK_GBS, "frac": roof["frac"],
+            "gate": 0.70, "avg_launch_ms": roof["avg_launch_ms"],
+            "algorithmic_bytes_per_launch": roof["algorithmic_bytes_per_launch"], "traffic": roof["traffic"],
+            "steps": steps}
+
+
+def selection_leg(dev, iters=100, warmup=5):
+    """Selection without collection on 2^22 Pareto(1.5) priorities, each
+    iteration a select of B = 8192 and an update of those draws:
+    prioritized with IS weights, then TopK of the 8192 highest.  Rated
+    against HBM with the bytes the method must move: the scan's 4N-byte read
+    of the priorities plus the select's outputs (idx 8 B, start 4 B, weight
+    4 B per draw), and for the update the idx and value read and the
+    priority written (16 B per draw)."""
+    from gen import configs
+    out = {}
+    for w, key in ((configs.SELECT_STRESS, "prioritized"), (configs.TOPK_STRESS, "topk")):
+        t = make_table(w)
+        try:
+            r = run_steps(t, w, iters, warmup, dev, pipelined=False, stage_steps=iters)
+        finally:
+            t.close()
+        sel_ms, upd_ms = r["stages_mean"]["select"], r["stages_mean"]["update"]
+        sel_bytes = 4 * w.N + w.B * (8 + 4 + (4 if w.weights else 0))
+        upd_bytes = 16 * w.B
+        out[key] = {"workload": w.name, "select_us": round(sel_ms * 1e3, 2), "update_us": round(upd_ms * 1e3, 2),
+                    "samples_per_s": round(w.B / (sel_ms * 1e-3), 1),
+                    "select_algorithmic_bytes": sel_bytes,
+                    "select_frac_of_hbm": round(sel_bytes / (sel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                    "update_algorithmic_bytes": upd_bytes,
+                    "update_frac_of_hbm": round(upd_bytes / (upd_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                    "select_us_p10_p50_p90": [round(x * 1e3, 2) for x in r["stages_pct"]["select"]],
+                    "iterations": iters}
+    return out
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -587,11 +872,8 @@ def main():
         run_shard(args)
         return
 
-    import numpy as np
     import torch
 
-    import gen
-    from gen.fill import fill_table
     from paper_2310_05205_amd import gear
 
     if not torch.cuda.is_available():
@@ -599,150 +881,74 @@ def main():
     gear.lib()  # fails loudly if the library is not built
     w = workload(args.workload)
     dev = torch.device("cuda", 0)
-    stream = torch.cuda.current_stream(dev)
-    sh = stream.cuda_stream
-
-    host_table = w.host_table
-    t = gear.Table(w.elem_bytes, w.N, w.T, gear.GEAR_HOST_PINNED if host_table else gear.GEAR_DEVICE, 0)
-    fill_table(w, lambda n, ptrs, prio: t.insert(ptrs, prio), device=0)
+    t = make_table(w)
     opts = (gear.GEAR_OPT_INCREMENTAL_TREE if args.incremental else 0) | \
         (gear.GEAR_OPT_IS_GLOBAL_MIN if args.global_min else 0)
     if opts:
         t.set_options(opts)
-
     K, W = args.steps, args.warmup
-    B, L = w.B, w.L
     strategy = w.strategies[0]
-    prioritized = strategy in (gear.GEAR_PRIORITIZED, gear.GEAR_TOPK)  # steps that update priorities
-    idx = torch.empty(B, dtype=torch.int64, device=dev)
-    start = torch.empty(B, dtype=torch.int32, device=dev)
-    wts = torch.empty(B, dtype=torch.float32, device=dev)
-    outs = [torch.empty(B * L * e, dtype=torch.uint8, device=dev) for e in w.elem_bytes]
-    out_ptrs = [o.data_ptr() for o in outs]
-    newp = torch.from_numpy(np.stack([gen.update_priorities(w.prio, w.seed, it, B) for it in range(W + K)])).to(dev)
-    seeds = [gen.select_seed(w.seed, it) for it in range(W + K)]
-    batch_bytes = B * L * sum(w.elem_bytes)
-
-    def step(it):
-        gear.gear_select(t.handle, strategy, B, L, seeds[it], w.beta, idx.data_ptr(), start.data_ptr(),
-                         wts.data_ptr() if w.weights else 0, sh)
-        if outs:
-            gear.gear_collect(t.handle, idx.data_ptr(), start.data_ptr(), B, L, None, out_ptrs, sh)
-        if prioritized:
-            gear.gear_update_priorities(t.handle, idx.data_ptr(), newp[it].data_ptr(), B, sh)
-
-    for it in range(W):
-        step(it)
-    torch.cuda.synchronize()
-    if t.sync() != 0:
-        raise SystemExit("device status set during warm-up")
-
-    # Timed region: K whole steps; HIP events on the same stream bracket each
-    # gather launch.
-    hev = HipEvents()
-    ev = [(hev.create(), hev.create()) for _ in range(K)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(K):
-        it = W + k
-        gear.gear_select(t.handle, strategy, B, L, seeds[it], w.beta, idx.data_ptr(), start.data_ptr(),
-                         wts.data_ptr() if w.weights else 0, sh)
-        hev.record(ev[k][0], sh)
-        if outs:
-            gear.gear_collect(t.handle, idx.data_ptr(), start.data_ptr(), B, L, None, out_ptrs, sh)
-        hev.record(ev[k][1], sh)
-        if prioritized:
-            gear.gear_update_priorities(t.handle, idx.data_ptr(), newp[it].data_ptr(), B, sh)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    status = t.sync()
-    if status != 0:
-        raise SystemExit("device status %d set during the timed steps" % status)
-    wall = t1 - t0
-    col_ms = float(np.mean([hev.elapsed_ms(a, b) for a, b in ev]))
-
-    # Stage breakdown, after the timed region (events around every stage).
-    nb = min(K, 50)
-    sev = [[hev.create() for _ in range(4)] for _ in range(nb)]
-    for k in range(nb):
-        it = W + k
-        e = sev[k]
-        hev.record(e[0], sh)
-        gear.gear_select(t.handle, strategy, B, L, seeds[it], w.beta, idx.data_ptr(), start.data_ptr(),
-                         wts.data_ptr() if w.weights else 0, sh)
-        hev.record(e[1], sh)
-        if outs:
-            gear.gear_collect(t.handle, idx.data_ptr(), start.data_ptr(), B, L, None, out_ptrs, sh)
-        hev.record(e[2], sh)
-        if prioritized:
-            gear.gear_update_priorities(t.handle, idx.data_ptr(), newp[it].data_ptr(), B, sh)
-        hev.record(e[3], sh)
-    torch.cuda.synchronize()
-    sel_all = [hev.elapsed_ms(e[0], e[1]) for e in sev]
-    col_all = [hev.elapsed_ms(e[1], e[2]) for e in sev]
-    upd_all = [hev.elapsed_ms(e[2], e[3]) for e in sev]
-    sel_ms = float(np.mean(sel_all))
-    upd_ms = float(np.mean(upd_all))
-    pct = {name: [round(float(x), 5) for x in np.percentile(v, [10, 50, 90])]
-           for name, v in (("select", sel_all), ("collect", col_all), ("update", upd_all))
-           if name != "update" or prioritized}
-    hev.close()
-
-    if host_table:
-        alg_bytes = batch_bytes                  # bytes crossing the host link
-        peak, bound = HOST_LINK_PEAK_GBS, "host-link"
-    else:
-        alg_bytes = 2 * batch_bytes              # window bytes read + batch bytes written
-        peak, bound = HBM_PEAK_GBS, "hbm"
-    roof = None
-    if outs:
-        achieved = alg_bytes / (col_ms * 1e-3) / 1e9
-        roof = {"bound": bound, "achieved": round(achieved, 1), "peak": peak, "unit": "GB/s",
-                "frac": round(achieved / peak, 4),
-                "traffic": profiled_traffic("collect_kernel", args.workload),
-                "kernel": "collect_kernel", "algorithmic_bytes_per_launch": alg_bytes,
-                "avg_launch_ms": round(col_ms, 5)}
-
-    context = torch_context(t, w, dev) if strategy in (gear.GEAR_PRIORITIZED, gear.GEAR_TOPK) else None
-
+    # Steps of a device table with columns are pipelined over two streams;
+    # a pinned host table's gather takes milliseconds, so its steps run in
+    # order on one stream, and so does a selection-only workload.
+    pipelined = bool(w.elem_bytes) and not w.host_table and not args.serial
+    r = run_steps(t, w, K, W, dev, pipelined, group=args.group, serial_too=pipelined)
+    prioritized = strategy in (gear.GEAR_PRIORITIZED, gear.GEAR_TOPK)
+    roof = gather_roofline(w, r["collect_ms"], args.workload) if w.elem_bytes else None
+    context = torch_context(t, w, dev) if prioritized else None
     link = None
-    if host_table and outs:
-        link = host_link_extras(t, w, idx, start, outs, dev)
+    if w.host_table and w.elem_bytes:
+        st = r["step"]
+        link = host_link_extras(t, w, st.idx[0], st.start[0], st.outs[0], dev)
         if not link["cpu_staged"]["matches_zero_copy"]:
             raise SystemExit("the CPU-staged batch differs from the zero-copy batch")
         link["zero_copy_frac_of_h2d_copy"] = round(roof["achieved"] / link["link_h2d_copy_gbs"], 4)
+    del r["step"]
+    t.close()
 
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, args.cpu_seconds, args.global_min)
 
-    steps_per_s = B * L * K / wall
+    B, L = w.B, w.L
+    sm = r["stages_mean"]
     line = {
-        "metric": METRIC, "value": round(steps_per_s, 1), "unit": "trajectory-steps/s", "n_gpus": 1,
-        "steps": K, "warmup": W, "ms_per_step": round(wall * 1e3 / K, 5), "higher_is_better": True,
+        "metric": METRIC, "value": round(B * L * K / r["wall_s"], 1), "unit": "trajectory-steps/s", "n_gpus": 1,
+        "steps": K, "warmup": W, "ms_per_step": round(r["wall_s"] * 1e3 / K, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "u64", "data": "synthetic",
         "config": {"workload": w.name, "N": w.N, "T": w.T, "B": B, "L": L,
                    "columns": {c.name: "%s[%d]" % (c.dtype, c.m) for c in w.columns},
                    "elem_bytes": w.elem_bytes, "table_bytes": w.table_bytes,
-                   "residency": "pinned-host" if host_table else "hbm",
+                   "residency": "pinned-host" if w.host_table else "hbm",
                    "strategy": {0: "fifo", 1: "lifo", 2: "uniform", 3: "prioritized", 4: "topk"}[strategy],
                    "is_weights": bool(w.weights), "parallelism": "1 GPU",
                    "tree": "incremental" if args.incremental and not args.global_min else "rescan per select",
-                   "is_normalisation": "table minimum" if args.global_min else "batch minimum"},
+                   "is_normalisation": "table minimum" if args.global_min else "batch minimum",
+                   "steps_issued": "two streams, select/update overlapping the gather" if pipelined
+                   else "one stream, in order", "batch_buffer_sets": r["buffer_sets"],
+                   "steps_per_handshake": args.group if pipelined else None},
         "roofline": roof,
         "cpu_baseline": cpu,
-        "stages_ms": {"select": round(sel_ms, 5), "collect": round(col_ms, 5),
-                      "update": round(upd_ms, 5) if prioritized else None,
-                      "note": "select/update from a separate loop after the timed region"},
-        "stages_ms_p10_p50_p90": pct,
-        "selection_samples_per_s": round(B / (sel_ms * 1e-3), 1),
-        "batch_bytes": batch_bytes,
+        "stages_ms": {"select": round(sm["select"], 5),
+                      "collect": round(sm["collect"], 5) if w.elem_bytes else None,
+                      "update": round(sm["update"], 5) if prioritized else None,
+                      "note": "from a one-stream loop with events around every stage, after the timed region"},
+        "stages_ms_p10_p50_p90": r["stages_pct"],
+        "selection_samples_per_s": round(B / (sm["select"] * 1e-3), 1),
+        "batch_bytes": B * L * sum(w.elem_bytes),
     }
+    if pipelined:
+        line["serial_ms_per_step"] = round(r["serial_ms_per_step"], 5)
+        line["serial_value"] = round(B * L / (r["serial_ms_per_step"] * 1e-3), 1)
     if link is not None:
         line["host_link"] = link
     if context is not None:
         line["torch_context"] = context
-    t.close()
+    if args.workload == "mat" and not (args.incremental or args.global_min) and args.legs == "all":
+        # The other gates, measured in the same run after the headline table is closed.
+        line["host_link"] = host_link_leg(dev)
+        line["dt_full"] = dt_full_leg(dev)
+        line["selection"] = selection_leg(dev)
     print(json.dumps(line), flush=True)
 
 
