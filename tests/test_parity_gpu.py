@@ -361,6 +361,9 @@ def test_device_status_and_host_errors():
 # ---------------------------------------------------------------------------
 
 def _full_size(w, iterations, sample_n, options=0):
+    """Every iteration compares all draws and weights; the first compares
+    every gathered window of the batch (the oracle regenerates all B selected
+    trajectories), later ones sample_n windows including the first and last."""
     p, next_seq = oracle_priorities(w)
     t = gpu_table(w, options=options)
     rng = np.random.default_rng(w.seed)
@@ -375,12 +378,16 @@ def _full_size(w, iterations, sample_n, options=0):
             np.testing.assert_array_equal(host(idx), oidx)
             np.testing.assert_array_equal(host(start), ostart)
             assert_weights(host(wt), ow)
-            sample = np.sort(rng.choice(w.B, size=sample_n, replace=False))
-            sample[0], sample[-1] = 0, w.B - 1
+            if it == 0:
+                sample = np.arange(w.B)
+            else:
+                sample = np.sort(rng.choice(w.B, size=sample_n, replace=False))
+                sample[0], sample[-1] = 0, w.B - 1
             ref = oracle_windows(w, oidx, ostart, w.L, next_seq, sample)
             for c in range(len(w.columns)):
-                np.testing.assert_array_equal(host(outs[c][torch.from_numpy(sample).to(cuda())]), ref[c])
-            del outs
+                got = host(outs[c]) if it == 0 else host(outs[c][torch.from_numpy(sample).to(cuda())])
+                np.testing.assert_array_equal(got, ref[c])
+            del outs, ref, got
             newp = gen.update_priorities(w.prio, w.seed, it, w.B)
             t.update_priorities(idx, torch.from_numpy(newp).to(cuda()))
             oracle.update(p, oidx, newp)
