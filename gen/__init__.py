@@ -64,8 +64,10 @@ _gpu = None
 def cpu_lib():
     global _cpu
     if _cpu is None:
-        build_cpu()
-        L = ctypes.CDLL(_CPU_LIB)
+        # GEN_CPU_LIB names another build of gen.c to load instead (the
+        # sanitizer test loads an instrumented build through it).
+        path = os.environ.get("GEN_CPU_LIB") or build_cpu()
+        L = ctypes.CDLL(path)
         L.gen_fill_rows_cpu.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64,
                                         ctypes.c_uint32, ctypes.c_int32, ctypes.c_uint64, ctypes.c_int64,
                                         ctypes.c_void_p]

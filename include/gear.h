@@ -41,6 +41,9 @@
  *     counters, whether the sum tree is current, which copy of its upper
  *     levels is live), so a replayed capture would repeat stale decisions:
  *     call them directly.
+ *   - A HIP error left pending by an earlier call outside the library (a
+ *     failed allocation, say) is cleared when a library call starts, so a
+ *     return code describes only that call's own work.
  *   - Conditions only the device can see (all priorities zero, an index or
  *     window start out of range) are recorded in the table's device status
  *     word, returned and cleared by gear_table_sync().
@@ -97,6 +100,34 @@ extern "C" {
 
 typedef struct gear_table gear_table;
 
+/* Element types of typed columns (gear_column.dtype).  The library moves
+ * bytes and never interprets them; the type fixes the element size and
+ * lets a binding hand out typed views of gathered batches. */
+#define GEAR_DTYPE_U8    0   /* 1 byte */
+#define GEAR_DTYPE_I8    1   /* 1 */
+#define GEAR_DTYPE_U16   2   /* 2 */
+#define GEAR_DTYPE_I16   3   /* 2 */
+#define GEAR_DTYPE_F16   4   /* 2, IEEE binary16 */
+#define GEAR_DTYPE_BF16  5   /* 2, bfloat16 */
+#define GEAR_DTYPE_U32   6   /* 4 */
+#define GEAR_DTYPE_I32   7   /* 4 */
+#define GEAR_DTYPE_F32   8   /* 4 */
+#define GEAR_DTYPE_U64   9   /* 8 */
+#define GEAR_DTYPE_I64  10   /* 8 */
+#define GEAR_DTYPE_F64  11   /* 8 */
+#define GEAR_MAX_NAME   63   /* longest column name, bytes */
+
+/* A typed column (Sec. 3.2, shard storage format: each field has a name and
+ * a fixed per-step shape, set when the store is created).  One step holds
+ * elems_per_step elements of dtype, i.e. elem_bytes = size(dtype) *
+ * elems_per_step; the per-step shape itself (for example 8 x 64) is the
+ * caller's, the library keeps only the element count. */
+typedef struct {
+    const char *name;        /* 1 .. GEAR_MAX_NAME bytes, unique in the table; copied */
+    int32_t dtype;           /* GEAR_DTYPE_* */
+    int32_t elems_per_step;  /* >= 1 */
+} gear_column;
+
 /*
  * gear_table_create - allocate an empty store (Sec. 3.2, shard storage
  * format: one column table per field type, each a contiguous array of
@@ -122,6 +153,34 @@ typedef struct gear_table gear_table;
  */
 int gear_table_create(const int64_t *elem_bytes, int32_t ncols, int64_t capacity, int32_t T,
                       int32_t residency, int32_t device, gear_table **out);
+
+/*
+ * gear_table_create_columns - gear_table_create with typed, named columns
+ * (Sec. 3.2: the storage format is defined by the fields and their shapes).
+ * Column c has elem_bytes = size(cols[c].dtype) * cols[c].elems_per_step and
+ * the same layout, residency and ownership as above; names and types are
+ * kept with the table (gear_table_column_info, gear_table_find_column).
+ *
+ *   cols   host array of ncols descriptors (0 .. GEAR_MAX_COLUMNS; the
+ *          strings are copied, so they need not outlive the call)
+ *
+ * Errors: GEAR_E_INVAL (NULL or repeated name, name too long, unknown dtype,
+ * elems_per_step < 1, and as gear_table_create), GEAR_E_NOMEM, GEAR_E_HIP.
+ */
+int gear_table_create_columns(const gear_column *cols, int32_t ncols, int64_t capacity, int32_t T,
+                              int32_t residency, int32_t device, gear_table **out);
+
+/* gear_table_column_info - name, dtype and elements per step of column c.
+ * A table made by gear_table_create has byte columns: name "c<index>",
+ * GEAR_DTYPE_U8, elems_per_step = elem_bytes.  *name stays valid while the
+ * table exists.  Any output may be NULL.  Errors: GEAR_E_INVAL. */
+int gear_table_column_info(const gear_table *t, int32_t c, const char **name, int32_t *dtype,
+                           int32_t *elems_per_step);
+
+/* gear_table_find_column - index of the column called `name` (for the
+ * col_ids of gear_collect).  Errors: GEAR_E_INVAL (NULL argument, no such
+ * column; *c is then -1). */
+int gear_table_find_column(const gear_table *t, const char *name, int32_t *c);
 
 /* gear_table_destroy - synchronize the table's device and free all its
  * memory.  NULL is accepted.  Errors: GEAR_E_HIP. */

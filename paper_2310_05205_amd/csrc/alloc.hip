@@ -326,10 +326,15 @@ extern "C" int gear_table_use_allocator(gear_table* h, int32_t removal, int64_t 
         return fail(GEAR_E_NOMEM, "gear_table_use_allocator: host index arrays");
     }
     for (int64_t i = 0; i < t->N; i++) t->free_q[(size_t)i] = (int32_t)i;  // every index free, in index order
-    hipError_t e;
-    if ((e = hipMalloc(reinterpret_cast<void**>(&t->order), sizeof(int32_t) * (size_t)t->N)) != hipSuccess ||
-        (e = hipMalloc(reinterpret_cast<void**>(&t->committed), (size_t)t->N)) != hipSuccess) {
+    hipError_t e = hipSuccess;
+    gear::AllocHook hook;
+    if ((e = hook.fail_next() ? hipErrorOutOfMemory
+                              : hipMalloc(reinterpret_cast<void**>(&t->order), sizeof(int32_t) * (size_t)t->N)) !=
+            hipSuccess ||
+        (e = hook.fail_next() ? hipErrorOutOfMemory : hipMalloc(reinterpret_cast<void**>(&t->committed), (size_t)t->N)) !=
+            hipSuccess) {
         gear::free_index_manager(*t);
+        (void)hipGetLastError();  // reported here, not by a later launch
         return fail(GEAR_E_NOMEM, "gear_table_use_allocator: device arrays");
     }
     if ((e = hipMemset(t->committed, 0, (size_t)t->N)) != hipSuccess ||

@@ -49,6 +49,9 @@ struct Table {
     int32_t T = 0;
     int32_t ncols = 0;
     std::vector<int64_t> elem_bytes;
+    std::vector<std::string> col_name;  // column names ("c<index>" for byte columns)
+    std::vector<int32_t> col_dtype;     // GEAR_DTYPE_* per column
+    std::vector<int32_t> col_elems;     // elements per step per column
     std::vector<uint8_t*> col_dev;    // device-visible base of each column
     std::vector<uint8_t*> col_host;   // host base (pinned tables), else null
 
@@ -107,6 +110,22 @@ struct Table {
 // Thread-local error reporting.
 int fail(int code, const std::string& msg);
 int hip_fail(hipError_t e, const char* what);
+
+// Allocation failures on demand, for tests of the cleanup paths: with
+// GEAR_TEST_FAIL_ALLOC=n (n >= 1) in the environment, the n-th allocation
+// made through one hook fails as if memory were exhausted.  Each
+// gear_table_create and gear_table_use_allocator call counts its own
+// allocations.  Without the variable nothing fails.
+class AllocHook {
+  public:
+    AllocHook();
+    // True when the next allocation is to fail.
+    bool fail_next() { return ++count_ == fail_at_; }
+
+  private:
+    long fail_at_ = 0;
+    long count_ = 0;
+};
 
 // Makes the table's device current for the lifetime of the guard.
 class DeviceGuard {

@@ -640,6 +640,7 @@ extern "C" int gear_select_prioritized_noalloc(const uint32_t* d_priority, int64
     if (B < 1 || B > GEAR_MAX_BATCH) return fail(GEAR_E_INVAL, "gear_select_prioritized_noalloc: B out of range");
     if (T < 1 || L < 1 || L > T) return fail(GEAR_E_INVAL, "gear_select_prioritized_noalloc: L must lie in [1, T]");
     if (!(beta == beta)) return fail(GEAR_E_INVAL, "gear_select_prioritized_noalloc: beta is NaN");
+    (void)hipGetLastError();  // an error pending from an earlier HIP call is not this call's
     int dev = -1;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "gear_select_prioritized_noalloc: hipGetDevice");

@@ -364,6 +364,7 @@ extern "C" int gear_topk_merge(const uint32_t* d_prio, const int64_t* d_gidx, in
     if (T < 1 || L < 1 || L > T) return fail(GEAR_E_INVAL, "gear_topk_merge: L must lie in [1, T]");
     if (d_prio == nullptr || d_gidx == nullptr || d_idx == nullptr || d_start == nullptr)
         return fail(GEAR_E_INVAL, "gear_topk_merge: NULL pointer argument");
+    (void)hipGetLastError();  // an error pending from an earlier HIP call is not this call's
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipLaunchKernelGGL(gear::merge_fill_kernel, dim3(gear::blocks_for(K)), dim3(256), 0, s, K, d_idx, d_start,
                        d_weights, d_out_prio);

@@ -1,6 +1,7 @@
 // Host runtime of the replay store: creation, insertion with FIFO removal,
 // status synchronisation and accessors (GEAR Sec. 3.2).
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <string>
@@ -26,6 +27,11 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 DeviceGuard::DeviceGuard(int dev) {
+    // Kernel launches are checked with hipGetLastError, which also returns
+    // an error left pending by any earlier HIP call of this thread (a failed
+    // allocation elsewhere, say).  Clear it, so that the call's return code
+    // describes only its own work.
+    (void)hipGetLastError();
     int cur = -1;
     err_ = hipGetDevice(&cur);
     if (err_ == hipSuccess && cur != dev) {
@@ -36,6 +42,11 @@ DeviceGuard::DeviceGuard(int dev) {
 
 DeviceGuard::~DeviceGuard() {
     if (prev_ >= 0) (void)hipSetDevice(prev_);
+}
+
+AllocHook::AllocHook() {
+    const char* v = getenv("GEAR_TEST_FAIL_ALLOC");
+    if (v != nullptr) fail_at_ = strtol(v, nullptr, 10);
 }
 
 }  // namespace gear
@@ -77,14 +88,87 @@ void free_table(Table* t) {
 }
 
 template <typename P>
-hipError_t dmalloc(P** p, size_t bytes) {
+hipError_t dmalloc(gear::AllocHook& hook, P** p, size_t bytes) {
+    if (hook.fail_next()) return hipErrorOutOfMemory;
     return hipMalloc(reinterpret_cast<void**>(p), bytes);
 }
+
+hipError_t hmalloc(gear::AllocHook& hook, void** p, size_t bytes, unsigned flags) {
+    if (hook.fail_next()) return hipErrorOutOfMemory;
+    return hipHostMalloc(p, bytes, flags);
+}
+
+}  // namespace
+
+namespace {
+
+int dtype_bytes(int32_t dtype) {
+    switch (dtype) {
+        case GEAR_DTYPE_U8: case GEAR_DTYPE_I8: return 1;
+        case GEAR_DTYPE_U16: case GEAR_DTYPE_I16: case GEAR_DTYPE_F16: case GEAR_DTYPE_BF16: return 2;
+        case GEAR_DTYPE_U32: case GEAR_DTYPE_I32: case GEAR_DTYPE_F32: return 4;
+        case GEAR_DTYPE_U64: case GEAR_DTYPE_I64: case GEAR_DTYPE_F64: return 8;
+        default: return 0;
+    }
+}
+
+// Column names, types and element counts of a new table; byte columns when
+// `cols` is NULL.
+struct ColumnMeta {
+    std::vector<std::string> name;
+    std::vector<int32_t> dtype, elems;
+};
+
+int create_table(const int64_t* elem_bytes, int32_t ncols, int64_t capacity, int32_t T, int32_t residency,
+                 int32_t device, gear_table** out, ColumnMeta meta);
 
 }  // namespace
 
 extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64_t capacity, int32_t T,
                                  int32_t residency, int32_t device, gear_table** out) {
+    ColumnMeta meta;
+    if (elem_bytes != nullptr && ncols > 0 && ncols <= GEAR_MAX_COLUMNS)
+        for (int c = 0; c < ncols; c++) {
+            meta.name.push_back("c" + std::to_string(c));
+            meta.dtype.push_back(GEAR_DTYPE_U8);
+            meta.elems.push_back((int32_t)(elem_bytes[c] > 0 && elem_bytes[c] <= (1ll << 30) ? elem_bytes[c] : 0));
+        }
+    return create_table(elem_bytes, ncols, capacity, T, residency, device, out, std::move(meta));
+}
+
+extern "C" int gear_table_create_columns(const gear_column* cols, int32_t ncols, int64_t capacity, int32_t T,
+                                         int32_t residency, int32_t device, gear_table** out) {
+    if (out == nullptr) return fail(GEAR_E_INVAL, "gear_table_create_columns: out is NULL");
+    *out = nullptr;
+    if (ncols < 0 || ncols > GEAR_MAX_COLUMNS)
+        return fail(GEAR_E_INVAL, "gear_table_create_columns: ncols out of range");
+    if (ncols > 0 && cols == nullptr) return fail(GEAR_E_INVAL, "gear_table_create_columns: cols is NULL");
+    ColumnMeta meta;
+    std::vector<int64_t> eb;
+    for (int c = 0; c < ncols; c++) {
+        if (cols[c].name == nullptr) return fail(GEAR_E_INVAL, "gear_table_create_columns: a column name is NULL");
+        const size_t len = strnlen(cols[c].name, GEAR_MAX_NAME + 1);
+        if (len == 0 || len > GEAR_MAX_NAME)
+            return fail(GEAR_E_INVAL, "gear_table_create_columns: a column name is empty or longer than GEAR_MAX_NAME");
+        std::string name(cols[c].name, len);
+        for (const std::string& other : meta.name)
+            if (other == name) return fail(GEAR_E_INVAL, "gear_table_create_columns: repeated column name " + name);
+        const int size = dtype_bytes(cols[c].dtype);
+        if (size == 0) return fail(GEAR_E_INVAL, "gear_table_create_columns: unknown dtype of column " + name);
+        if (cols[c].elems_per_step < 1)
+            return fail(GEAR_E_INVAL, "gear_table_create_columns: elems_per_step < 1 in column " + name);
+        meta.name.push_back(name);
+        meta.dtype.push_back(cols[c].dtype);
+        meta.elems.push_back(cols[c].elems_per_step);
+        eb.push_back((int64_t)size * cols[c].elems_per_step);
+    }
+    return create_table(eb.data(), ncols, capacity, T, residency, device, out, std::move(meta));
+}
+
+namespace {
+
+int create_table(const int64_t* elem_bytes, int32_t ncols, int64_t capacity, int32_t T, int32_t residency,
+                 int32_t device, gear_table** out, ColumnMeta meta) {
     if (out == nullptr) return fail(GEAR_E_INVAL, "gear_table_create: out is NULL");
     *out = nullptr;
     if (ncols < 0 || ncols > GEAR_MAX_COLUMNS) return fail(GEAR_E_INVAL, "gear_table_create: ncols out of range");
@@ -113,6 +197,7 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
     if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
         return fail(GEAR_E_INVAL, std::string("gear_table_create: library is built for gfx950, device is ") + prop.gcnArchName);
 
+    gear::AllocHook hook;
     Table* t = new Table();
     t->device = device;
     t->residency = residency;
@@ -120,11 +205,15 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
     t->T = T;
     t->ncols = ncols;
     t->elem_bytes.assign(elem_bytes, elem_bytes + ncols);
+    t->col_name = std::move(meta.name);
+    t->col_dtype = std::move(meta.dtype);
+    t->col_elems = std::move(meta.elems);
     t->col_dev.assign(ncols, nullptr);
     t->col_host.assign(ncols, nullptr);
 
     auto oom = [&](const char* what, hipError_t err) {
         free_table(t);
+        (void)hipGetLastError();  // the failed allocation's error is reported here, not by a later launch
         std::string m = std::string("gear_table_create: allocation of ") + what + " failed: " + hipGetErrorString(err);
         return fail(GEAR_E_NOMEM, m);
     };
@@ -132,7 +221,7 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
     for (int c = 0; c < ncols; c++) {
         size_t bytes = (size_t)capacity * (size_t)T * (size_t)elem_bytes[c];
         if (residency == GEAR_DEVICE) {
-            e = hipMalloc(reinterpret_cast<void**>(&t->col_dev[c]), bytes);
+            e = dmalloc(hook, &t->col_dev[c], bytes);
             if (e != hipSuccess) return oom("a device column", e);
             // Slots never inserted read as zeros.
             e = hipMemsetAsync(t->col_dev[c], 0, bytes, nullptr);
@@ -145,7 +234,7 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
             // (non-coherent) so the GPU may cache lines it reads; the table is
             // only written by insertion, ordered on the stream.
             void* h = nullptr;
-            e = hipHostMalloc(&h, bytes, hipHostMallocMapped | hipHostMallocNonCoherent);
+            e = hmalloc(hook, &h, bytes, hipHostMallocMapped | hipHostMallocNonCoherent);
             if (e != hipSuccess) return oom("a pinned host column", e);
             t->col_host[c] = static_cast<uint8_t*>(h);
             void* d = nullptr;
@@ -173,25 +262,25 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
         if (sz <= gear::kFanout) break;
         sz = (sz + gear::kFanout - 1) / gear::kFanout;
     }
-    if ((e = dmalloc(&t->priority, sizeof(uint32_t) * capacity)) != hipSuccess) return oom("priorities", e);
-    if ((e = dmalloc(&t->tag, sizeof(uint32_t) * capacity)) != hipSuccess) return oom("scatter tags", e);
-    if ((e = dmalloc(&t->tile_sums, sizeof(uint64_t) * t->ntiles)) != hipSuccess) return oom("tile sums", e);
+    if ((e = dmalloc(hook, &t->priority, sizeof(uint32_t) * capacity)) != hipSuccess) return oom("priorities", e);
+    if ((e = dmalloc(hook, &t->tag, sizeof(uint32_t) * capacity)) != hipSuccess) return oom("scatter tags", e);
+    if ((e = dmalloc(hook, &t->tile_sums, sizeof(uint64_t) * t->ntiles)) != hipSuccess) return oom("tile sums", e);
     for (int c = 0; c < 2; c++)
         for (int l = 1; l < t->nlevels; l++) {
-            if ((e = dmalloc(&t->upper[c][l], sizeof(uint64_t) * t->level_size[l])) != hipSuccess)
+            if ((e = dmalloc(hook, &t->upper[c][l], sizeof(uint64_t) * t->level_size[l])) != hipSuccess)
                 return oom("sum tree levels", e);
             if ((e = hipMemset(t->upper[c][l], 0, sizeof(uint64_t) * t->level_size[l])) != hipSuccess) {
                 free_table(t);
                 return hip_fail(e, "gear_table_create: clearing the sum tree");
             }
         }
-    if ((e = dmalloc(&t->wg_min, sizeof(uint32_t) * gear::kSearchMaxGrid)) != hipSuccess) return oom("batch minima", e);
-    if ((e = dmalloc(&t->chunk_min, sizeof(uint32_t) * t->nchunks)) != hipSuccess) return oom("chunk minima", e);
-    if ((e = dmalloc(&t->status, sizeof(uint32_t))) != hipSuccess) return oom("status word", e);
+    if ((e = dmalloc(hook, &t->wg_min, sizeof(uint32_t) * gear::kSearchMaxGrid)) != hipSuccess) return oom("batch minima", e);
+    if ((e = dmalloc(hook, &t->chunk_min, sizeof(uint32_t) * t->nchunks)) != hipSuccess) return oom("chunk minima", e);
+    if ((e = dmalloc(hook, &t->status, sizeof(uint32_t))) != hipSuccess) return oom("status word", e);
     // Staging for host index and priority lists (row writes, index manager).
-    if ((e = dmalloc(&t->stage_idx, sizeof(int64_t) * gear::kStageRows)) != hipSuccess ||
-        (e = hipHostMalloc(reinterpret_cast<void**>(&t->pin_host), (size_t)(gear::kStageSlotBytes * gear::kStageSlots),
-                           hipHostMallocMapped | hipHostMallocCoherent)) != hipSuccess)
+    if ((e = dmalloc(hook, &t->stage_idx, sizeof(int64_t) * gear::kStageRows)) != hipSuccess ||
+        (e = hmalloc(hook, reinterpret_cast<void**>(&t->pin_host), (size_t)(gear::kStageSlotBytes * gear::kStageSlots),
+                     hipHostMallocMapped | hipHostMallocCoherent)) != hipSuccess)
         return oom("index staging", e);
     {
         void* d = nullptr;
@@ -203,11 +292,11 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
             free_table(t);
             return hip_fail(e, "gear_table_create: staging events");
         }
-    if ((e = dmalloc(&t->topk_hist, sizeof(uint32_t) * 3 * gear::kTopkBins)) != hipSuccess ||
-        (e = dmalloc(&t->topk_state, sizeof(uint32_t) * gear::kTopkStateWords)) != hipSuccess ||
-        (e = dmalloc(&t->topk_local, sizeof(uint32_t) * 3 * gear::kTopkMaxGrid * gear::kTopkBins)) != hipSuccess ||
-        (e = dmalloc(&t->topk_keys, sizeof(uint64_t) * gear::kTopkMaxK)) != hipSuccess ||
-        (e = dmalloc(&t->topk_rank, sizeof(uint32_t) * gear::kTopkMaxK)) != hipSuccess)
+    if ((e = dmalloc(hook, &t->topk_hist, sizeof(uint32_t) * 3 * gear::kTopkBins)) != hipSuccess ||
+        (e = dmalloc(hook, &t->topk_state, sizeof(uint32_t) * gear::kTopkStateWords)) != hipSuccess ||
+        (e = dmalloc(hook, &t->topk_local, sizeof(uint32_t) * 3 * gear::kTopkMaxGrid * gear::kTopkBins)) != hipSuccess ||
+        (e = dmalloc(hook, &t->topk_keys, sizeof(uint64_t) * gear::kTopkMaxK)) != hipSuccess ||
+        (e = dmalloc(hook, &t->topk_rank, sizeof(uint32_t) * gear::kTopkMaxK)) != hipSuccess)
         return oom("TopK scratch", e);
 
     if ((e = hipMemset(t->priority, 0, sizeof(uint32_t) * capacity)) != hipSuccess ||
@@ -224,6 +313,8 @@ extern "C" int gear_table_create(const int64_t* elem_bytes, int32_t ncols, int64
     *out = reinterpret_cast<gear_table*>(t);
     return GEAR_OK;
 }
+
+}  // namespace
 
 extern "C" int gear_table_destroy(gear_table* h) {
     if (h == nullptr) return GEAR_OK;
@@ -323,6 +414,29 @@ extern "C" int gear_table_column(const gear_table* h, int32_t c, void** base, vo
     if (host_ptr) *host_ptr = t->col_host[c];
     if (elem_bytes) *elem_bytes = t->elem_bytes[c];
     return GEAR_OK;
+}
+
+extern "C" int gear_table_column_info(const gear_table* h, int32_t c, const char** name, int32_t* dtype,
+                                      int32_t* elems_per_step) {
+    if (h == nullptr) return fail(GEAR_E_INVAL, "gear_table_column_info: table is NULL");
+    const Table* t = reinterpret_cast<const Table*>(h);
+    if (c < 0 || c >= t->ncols) return fail(GEAR_E_INVAL, "gear_table_column_info: no such column");
+    if (name) *name = t->col_name[c].c_str();
+    if (dtype) *dtype = t->col_dtype[c];
+    if (elems_per_step) *elems_per_step = t->col_elems[c];
+    return GEAR_OK;
+}
+
+extern "C" int gear_table_find_column(const gear_table* h, const char* name, int32_t* c) {
+    if (c != nullptr) *c = -1;
+    if (h == nullptr || name == nullptr || c == nullptr) return fail(GEAR_E_INVAL, "gear_table_find_column: NULL argument");
+    const Table* t = reinterpret_cast<const Table*>(h);
+    for (int j = 0; j < t->ncols; j++)
+        if (t->col_name[j] == name) {
+            *c = j;
+            return GEAR_OK;
+        }
+    return fail(GEAR_E_INVAL, std::string("gear_table_find_column: no column called ") + name);
 }
 
 extern "C" int gear_table_priorities(const gear_table* h, uint32_t** d_priority) {

@@ -38,6 +38,22 @@ GEAR_NOALLOC_MAX_N = 1 << 24
 GEAR_NOALLOC_SCRATCH_BYTES = 536832
 GEAR_OPT_INCREMENTAL_TREE = 1
 GEAR_OPT_IS_GLOBAL_MIN = 2
+GEAR_DTYPE_U8, GEAR_DTYPE_I8, GEAR_DTYPE_U16, GEAR_DTYPE_I16, GEAR_DTYPE_F16, GEAR_DTYPE_BF16 = 0, 1, 2, 3, 4, 5
+GEAR_DTYPE_U32, GEAR_DTYPE_I32, GEAR_DTYPE_F32, GEAR_DTYPE_U64, GEAR_DTYPE_I64, GEAR_DTYPE_F64 = 6, 7, 8, 9, 10, 11
+GEAR_MAX_NAME = 63
+# torch dtype name of each GEAR_DTYPE_* (the library only moves bytes).
+DTYPE_NAMES = {GEAR_DTYPE_U8: "uint8", GEAR_DTYPE_I8: "int8", GEAR_DTYPE_U16: "uint16", GEAR_DTYPE_I16: "int16",
+               GEAR_DTYPE_F16: "float16", GEAR_DTYPE_BF16: "bfloat16", GEAR_DTYPE_U32: "uint32",
+               GEAR_DTYPE_I32: "int32", GEAR_DTYPE_F32: "float32", GEAR_DTYPE_U64: "uint64", GEAR_DTYPE_I64: "int64",
+               GEAR_DTYPE_F64: "float64"}
+DTYPE_BYTES = {GEAR_DTYPE_U8: 1, GEAR_DTYPE_I8: 1, GEAR_DTYPE_U16: 2, GEAR_DTYPE_I16: 2, GEAR_DTYPE_F16: 2,
+               GEAR_DTYPE_BF16: 2, GEAR_DTYPE_U32: 4, GEAR_DTYPE_I32: 4, GEAR_DTYPE_F32: 4, GEAR_DTYPE_U64: 8,
+               GEAR_DTYPE_I64: 8, GEAR_DTYPE_F64: 8}
+
+
+class gear_column(ctypes.Structure):
+    """Mirror of the C descriptor gear_column."""
+    _fields_ = [("name", ctypes.c_char_p), ("dtype", ctypes.c_int32), ("elems_per_step", ctypes.c_int32)]
 
 
 class GearError(RuntimeError):
@@ -80,12 +96,18 @@ def lib():
         L.gear_is_weights.argtypes = [vp, vp, i32, ctypes.c_float, vp, vp]
         L.gear_topk_merge.argtypes = [vp, vp, i32, i32, i32, i32, u64, vp, vp, vp, vp, vp]
         L.gear_select_prioritized_noalloc.argtypes = [vp, i64, i32, i32, i32, u64, ctypes.c_float, vp, vp, vp, vp]
+        L.gear_table_create_columns.argtypes = [ctypes.POINTER(gear_column), i32, i64, i32, i32, i32,
+                                                ctypes.POINTER(vp)]
+        L.gear_table_column_info.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(i32),
+                                             ctypes.POINTER(i32)]
+        L.gear_table_find_column.argtypes = [vp, ctypes.c_char_p, ctypes.POINTER(i32)]
         for name in ["gear_table_create", "gear_table_destroy", "gear_insert", "gear_select", "gear_collect",
                      "gear_update_priorities", "gear_table_sync", "gear_table_info", "gear_table_column",
                      "gear_table_priorities", "gear_table_set_options", "gear_table_use_allocator",
                      "gear_allocate", "gear_commit", "gear_allocator_info", "gear_write_rows", "gear_shard_total",
                      "gear_select_shard", "gear_is_weights", "gear_topk_merge",
-                     "gear_select_prioritized_noalloc"]:
+                     "gear_select_prioritized_noalloc", "gear_table_create_columns", "gear_table_column_info",
+                     "gear_table_find_column"]:
             getattr(L, name).restype = ctypes.c_int
         L.gear_last_error.argtypes = []
         L.gear_last_error.restype = ctypes.c_char_p
@@ -116,6 +138,33 @@ def gear_table_create(elem_bytes, capacity, T, residency=GEAR_DEVICE, device=0):
     _check(lib().gear_table_create(eb, len(elem_bytes), int(capacity), int(T), int(residency), int(device),
                                    ctypes.byref(out)))
     return out.value
+
+
+def gear_table_create_columns(columns, capacity, T, residency=GEAR_DEVICE, device=0):
+    """columns: list of (name, GEAR_DTYPE_*, elems_per_step)."""
+    arr = (gear_column * max(len(columns), 1))()
+    keep = []
+    for i, (name, dtype, elems) in enumerate(columns):
+        b = name.encode()
+        keep.append(b)
+        arr[i] = gear_column(b, int(dtype), int(elems))
+    out = ctypes.c_void_p()
+    _check(lib().gear_table_create_columns(arr, len(columns), int(capacity), int(T), int(residency), int(device),
+                                           ctypes.byref(out)))
+    return out.value
+
+
+def gear_table_column_info(table, c):
+    name = ctypes.c_char_p()
+    dtype, elems = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(lib().gear_table_column_info(table, int(c), ctypes.byref(name), ctypes.byref(dtype), ctypes.byref(elems)))
+    return name.value.decode(), dtype.value, elems.value
+
+
+def gear_table_find_column(table, name):
+    c = ctypes.c_int32(-1)
+    _check(lib().gear_table_find_column(table, name.encode(), ctypes.byref(c)))
+    return c.value
 
 
 def gear_table_destroy(table):
@@ -256,21 +305,73 @@ class _DeviceBytes:
                                          "strides": None, "version": 2}
 
 
+def _dtype_code(dtype):
+    """GEAR_DTYPE_* of a torch dtype, a dtype name ("bfloat16", "bf16", ...) or a code."""
+    if isinstance(dtype, int):
+        return dtype
+    name = str(dtype).replace("torch.", "")
+    alias = {"u8": "uint8", "i8": "int8", "u16": "uint16", "i16": "int16", "f16": "float16", "half": "float16",
+             "bf16": "bfloat16", "u32": "uint32", "i32": "int32", "f32": "float32", "float": "float32",
+             "u64": "uint64", "i64": "int64", "f64": "float64", "double": "float64"}
+    name = alias.get(name, name)
+    for code, n in DTYPE_NAMES.items():
+        if n == name:
+            return code
+    raise ValueError("no GEAR dtype for %r" % (dtype,))
+
+
+class ColumnSpec:
+    """One typed column: name, GEAR_DTYPE_* code, per-step shape."""
+
+    def __init__(self, name, dtype, shape):
+        self.name = str(name)
+        self.dtype = _dtype_code(dtype)
+        self.shape = tuple(int(x) for x in shape)
+        n = 1
+        for x in self.shape:
+            n *= x
+        self.elems = n
+        self.elem_bytes = n * DTYPE_BYTES[self.dtype]
+
+    def torch_dtype(self):
+        import torch
+        return getattr(torch, DTYPE_NAMES[self.dtype])
+
+
 class Table:
     """A replay store over torch tensors.
 
-    ``columns`` is a list of bytes-per-step sizes.  Outputs are allocated as
-    torch CUDA tensors on the table's device; work is issued on torch's
-    current stream of that device.
+    ``columns`` is a list of bytes-per-step sizes (byte columns), or of typed
+    columns: (name, dtype, per-step shape) tuples or ColumnSpec objects, or a
+    dict {name: (dtype, shape)}.  Outputs are allocated as torch CUDA tensors
+    on the table's device; work is issued on torch's current stream of that
+    device.
     """
 
-    def __init__(self, elem_bytes, capacity, T, residency=GEAR_DEVICE, device=0):
+    def __init__(self, columns, capacity, T, residency=GEAR_DEVICE, device=0):
         import torch
         self._torch = torch
-        self.elem_bytes = [int(e) for e in elem_bytes]
+        if isinstance(columns, dict):
+            columns = [(name, spec[0], spec[1]) for name, spec in columns.items()]
+        columns = list(columns)
         self.capacity, self.T, self.device = int(capacity), int(T), int(device)
         self.residency = residency
-        self.handle = gear_table_create(self.elem_bytes, capacity, T, residency, device)
+        typed = not all(isinstance(c, int) for c in columns)
+        if typed:
+            specs = [c if isinstance(c, ColumnSpec) else ColumnSpec(*c) for c in columns]
+            self.elem_bytes = [c.elem_bytes for c in specs]
+            self.handle = gear_table_create_columns([(c.name, c.dtype, c.elems) for c in specs], capacity, T,
+                                                    residency, device)
+        else:
+            self.elem_bytes = [int(e) for e in columns]
+            self.handle = gear_table_create(self.elem_bytes, capacity, T, residency, device)
+        # Names, types and shapes as the library keeps them (byte columns:
+        # "c<index>", uint8, shape (elem_bytes,)); typed specs keep their shape.
+        self.columns = []
+        for c in range(len(self.elem_bytes)):
+            name, dtype, elems = gear_table_column_info(self.handle, c)
+            self.columns.append(ColumnSpec(name, dtype, specs[c].shape if typed else (elems,)))
+        self._index = {c.name: i for i, c in enumerate(self.columns)}
 
     def close(self):
         if self.handle:
@@ -288,11 +389,25 @@ class Table:
             return stream.cuda_stream
         return self._torch.cuda.current_stream(self.device).cuda_stream
 
+    def _sources(self, col_src):
+        """Pointers of the column sources, in column order: a list, or a dict
+        keyed by column name (every column; contiguous tensors or arrays)."""
+        if isinstance(col_src, dict):
+            missing = [c.name for c in self.columns if c.name not in col_src]
+            if missing:
+                raise ValueError("no source for columns %s" % missing)
+            col_src = [col_src[c.name] for c in self.columns]
+        for x in col_src:
+            if hasattr(x, "is_contiguous") and not x.is_contiguous():
+                raise ValueError("column sources must be contiguous")
+        return [_data_ptr(x) for x in col_src]
+
     def insert(self, col_src, priorities, stream=None):
-        """col_src: list of tensors/arrays [n, T*E_c] bytes (host or device); priorities uint32[n]."""
+        """col_src: per column, [n, T, *shape] data ([n, T*E_c] bytes for byte
+        columns), host or device, as a list in column order or a dict keyed by
+        name; priorities uint32[n]."""
         n = int(priorities.shape[0])
-        ptrs = [_data_ptr(x) for x in col_src]
-        gear_insert(self.handle, n, ptrs, _data_ptr(priorities), self._stream(stream))
+        gear_insert(self.handle, n, self._sources(col_src), _data_ptr(priorities), self._stream(stream))
 
     def select(self, strategy, B, L, seed, beta=0.0, weights=False, stream=None):
         torch = self._torch
@@ -315,6 +430,26 @@ class Table:
         gear_collect(self.handle, idx.data_ptr(), start.data_ptr(), B, L, col_ids,
                      [o.data_ptr() for o in out], self._stream(stream))
         return out
+
+    def collect_fields(self, idx, start, L, fields=None, stream=None, out=None):
+        """The batch as {name: tensor[B, L, *shape]} of each column's dtype
+        (Sec. 3.4: collect(indices, fields) handed over as tensors).  The
+        tensors are views of the byte batches that gear_collect writes (no
+        copy, no arithmetic); `out`, if given, is the dict of byte buffers
+        [B, L*E] to reuse."""
+        names = [c.name for c in self.columns] if fields is None else list(fields)
+        ids = [self._index[n] for n in names]
+        raw = self.collect(idx, start, L, col_ids=ids, stream=stream,
+                           out=None if out is None else [out[n] for n in names])
+        B = int(idx.shape[0])
+        res = {}
+        for n, c, r in zip(names, ids, raw):
+            spec = self.columns[c]
+            res[n] = r.view(spec.torch_dtype()).view((B, L) + spec.shape)
+        return res
+
+    def column_index(self, name):
+        return gear_table_find_column(self.handle, name)
 
     def update_priorities(self, idx, new_priorities, stream=None):
         gear_update_priorities(self.handle, idx.data_ptr(), new_priorities.data_ptr(), int(idx.shape[0]),
@@ -339,8 +474,9 @@ class Table:
         return gear_allocator_info(self.handle)
 
     def write_rows(self, idx, col_src, stream=None):
-        """Write row r of each column source (tensors/arrays [n, T*E_c]) into slot idx[r]."""
-        gear_write_rows(self.handle, idx, [_data_ptr(x) for x in col_src], self._stream(stream))
+        """Write row r of each column source ([n, T, *shape] per column, a list
+        or a dict keyed by name) into slot idx[r]."""
+        gear_write_rows(self.handle, idx, self._sources(col_src), self._stream(stream))
 
     def shard_total(self, out, stream=None):
         """Writes this table's priority total into `out` (a one-element int64

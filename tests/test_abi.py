@@ -81,6 +81,41 @@ def test_argument_validation_without_device():
     assert e.value.code == gear.GEAR_E_INVAL
 
 
+def test_typed_column_descriptors_are_validated_without_device():
+    lib = gear.lib()
+    out = ctypes.c_void_p()
+
+    def create(cols):
+        arr = (gear.gear_column * max(len(cols), 1))(*[gear.gear_column(n, d, e) for n, d, e in cols])
+        return lib.gear_table_create_columns(arr, len(cols), 16, 4, 0, 0, ctypes.byref(out))
+
+    assert create([(None, gear.GEAR_DTYPE_F32, 1)]) == gear.GEAR_E_INVAL
+    assert "NULL" in gear.gear_last_error()
+    assert create([(b"", gear.GEAR_DTYPE_F32, 1)]) == gear.GEAR_E_INVAL
+    assert create([(b"x" * (gear.GEAR_MAX_NAME + 1), gear.GEAR_DTYPE_F32, 1)]) == gear.GEAR_E_INVAL
+    assert create([(b"obs", gear.GEAR_DTYPE_F32, 1), (b"obs", gear.GEAR_DTYPE_I32, 2)]) == gear.GEAR_E_INVAL
+    assert "repeated" in gear.gear_last_error()
+    assert create([(b"obs", 12, 1)]) == gear.GEAR_E_INVAL
+    assert create([(b"obs", -1, 1)]) == gear.GEAR_E_INVAL
+    assert create([(b"obs", gear.GEAR_DTYPE_BF16, 0)]) == gear.GEAR_E_INVAL
+    assert lib.gear_table_create_columns(None, 1, 16, 4, 0, 0, ctypes.byref(out)) == gear.GEAR_E_INVAL
+    assert lib.gear_table_create_columns(None, 0, 16, 4, 0, 0, None) == gear.GEAR_E_INVAL
+    c = ctypes.c_int32(5)
+    assert lib.gear_table_find_column(None, b"obs", ctypes.byref(c)) == gear.GEAR_E_INVAL and c.value == -1
+    assert lib.gear_table_column_info(None, 0, None, None, None) == gear.GEAR_E_INVAL
+
+
+def test_column_specs_map_torch_dtypes():
+    spec = gear.ColumnSpec("obs", "bfloat16", (8, 64))
+    assert spec.dtype == gear.GEAR_DTYPE_BF16 and spec.elems == 512 and spec.elem_bytes == 1024
+    assert gear.ColumnSpec("a", "i32", (8,)).elem_bytes == 32
+    assert gear.ColumnSpec("r", "float32", ()).elem_bytes == 4
+    for code, name in gear.DTYPE_NAMES.items():
+        assert gear._dtype_code(name) == code and gear._dtype_code("torch." + name) == code
+    with pytest.raises(ValueError):
+        gear._dtype_code("complex64")
+
+
 def test_product_has_no_oracle_or_fallback():
     """The product package must not reach the oracle or a CPU path."""
     pkg = os.path.join(ROOT, "paper_2310_05205_amd")
