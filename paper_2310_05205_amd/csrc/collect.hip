@@ -6,11 +6,15 @@
 //     base_c + (idx[b]*T + start[b]) * E_c,  length W_c = L * E_c,
 // and each column's batch [B][L][E_c] is one contiguous range, so the copy
 // is driven by the output: a workgroup owns a contiguous piece of one
-// column's output.  Wide windows (W_c at least a piece) are split into
-// pieces; narrow windows are packed several to a piece with their source
-// offsets staged in LDS.  All requested columns run in one launch.  A column
-// table in pinned host memory is read by the same kernel through its mapped
-// address, so the loads go over the host link without a CPU copy.
+// column's output.  Wide columns (a window at least a piece long) are cut
+// into equal pieces of the whole batch, so a piece may run from the end of
+// one window into the start of the next (never further); a launch of a few
+// hundred MB then runs in equal pieces instead of ending on the short last
+// pieces of every window.  Narrow windows are packed several to a piece with
+// their source offsets staged in LDS.  All requested columns run in one
+// launch.  A column table in pinned host memory is read by the same kernel
+// through its mapped address, so the loads go over the host link without a
+// CPU copy.
 //
 // Element width per column: 16 bytes when every window source and output
 // address is 16-byte aligned, else 4 bytes when 4-byte aligned, else 1.
@@ -22,7 +26,13 @@ namespace gear {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;          // elements in flight per thread
+// Elements in flight per thread.  HBM tables: 8, pieces of 32 KiB at 16-byte
+// elements (a 102 MB launch of whole DT-shaped trajectories then runs in
+// about one round of resident workgroups: 20.1 against 21.3 us with 16 KiB
+// pieces).  Pinned host tables: 4, pieces of 16 KiB (32 KiB pieces read the
+// host link 4% slower).
+constexpr int kUnrollDevice = 8;
+constexpr int kUnrollHost = 4;
 constexpr int kMaxLaunchCols = 16;  // columns per launch (more take several launches)
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -33,10 +43,11 @@ struct ColTask {
     int64_t E;            // bytes per step
     int64_t W;            // window bytes, L*E
     int64_t task0;        // first task (workgroup) of this column
-    int64_t piece;        // bytes per piece: kThreads * kUnroll * width
-    int64_t ppw;          // pieces per window (wide columns)
+    int64_t piece;        // bytes per piece: kThreads * unroll * width
+    int64_t n;            // elements per window, W / width
     int32_t width;        // element bytes: 16, 4 or 1
-    int32_t wide;         // 1: pieces of one window; 0: several windows per piece
+    int32_t wide;         // 1: equal pieces of the batch, each within one or two windows;
+                          // 0: several whole windows per piece
     int32_t wpp;          // windows per piece (narrow)
     uint32_t epw;         // elements per window (narrow)
     uint32_t magic;       // ceil(2^32 / epw) for epw > 1: exact quotient for operands < 2^16
@@ -105,33 +116,58 @@ __device__ inline int64_t window_offset(const CollectArgs& a, const ColTask& c, 
     return (i * a.T + s) * c.E;
 }
 
-template <int WIDTH>
+// Piece q of a wide column: output elements [q*P, q*P + m) of the column's
+// batch, P = kThreads * U, m = P except in the batch's last piece.  A
+// window has n >= P elements, so the piece lies in window w0 from element r0
+// on and, if r0 + m > n, runs into window w0 + 1.
+template <int WIDTH, int U>
 __device__ void copy_wide(const CollectArgs& a, const ColTask& c, int64_t q) {
     typedef typename Elem<WIDTH>::type V;
-    const int64_t b = q / c.ppw;
-    const int64_t off0 = (q - b * c.ppw) * c.piece;
-    const int64_t len = (c.W - off0) < c.piece ? (c.W - off0) : c.piece;
-    const int64_t n = len / WIDTH;
-    V* dst = reinterpret_cast<V*>(c.out + b * c.W + off0);
-    const int64_t so = window_offset(a, c, b);
-    if (so < 0) {
-        for (int64_t e = threadIdx.x; e < n; e += kThreads) store_stream<WIDTH>(dst + e, zero_elem<WIDTH>());
-        if (threadIdx.x == 0 && so == kBadWindow) atomicOr(a.status, GEAR_STATUS_BAD_INDEX);
+    constexpr int64_t P = (int64_t)kThreads * U;
+    const int64_t o0 = q * P;
+    const int64_t w0 = o0 / c.n;
+    const int64_t r0 = o0 - w0 * c.n;
+    const int64_t total = (int64_t)a.B * c.n;
+    const int64_t m = (total - o0) < P ? (total - o0) : P;
+    const bool two = r0 + m > c.n;
+    const int64_t so0 = window_offset(a, c, w0);
+    const int64_t so1 = two ? window_offset(a, c, w0 + 1) : kNoWindow;
+    if (threadIdx.x == 0 && (so0 == kBadWindow || so1 == kBadWindow)) atomicOr(a.status, GEAR_STATUS_BAD_INDEX);
+    const V* src = reinterpret_cast<const V*>(c.src);
+    V* dst = reinterpret_cast<V*>(c.out) + o0;
+    // Element offsets of the two windows' sources, shifted so that element
+    // r of the piece (r = r0 + e) reads base + r in either window.
+    const int64_t b0 = so0 / WIDTH, b1 = so1 / WIDTH - c.n;
+    V v[U];
+    if (m == P && so0 >= 0 && (!two || so1 >= 0)) {
+        // Every element valid: the loads go out unconditionally, all in flight.
+#pragma unroll
+        for (int k = 0; k < U; k++) {
+            const int64_t r = r0 + threadIdx.x + k * kThreads;
+            v[k] = load_stream<WIDTH>(src + (r < c.n ? b0 : b1) + r);
+        }
+#pragma unroll
+        for (int k = 0; k < U; k++) store_stream<WIDTH>(dst + threadIdx.x + k * kThreads, v[k]);
         return;
     }
-    const V* src = reinterpret_cast<const V*>(c.src + so + off0);
-    if (n == (int64_t)kThreads * kUnroll) {
-        V v[kUnroll];
+    // The batch's last piece, or a piece touching a missing or invalid
+    // window (whose elements are zero).
 #pragma unroll
-        for (int k = 0; k < kUnroll; k++) v[k] = load_stream<WIDTH>(src + threadIdx.x + k * kThreads);
+    for (int k = 0; k < U; k++) {
+        const int64_t e = threadIdx.x + k * kThreads;
+        const int64_t r = r0 + e;
+        const bool second = r >= c.n;
+        v[k] = zero_elem<WIDTH>();
+        if (e < m && (second ? so1 : so0) >= 0) v[k] = load_stream<WIDTH>(src + (second ? b1 : b0) + r);
+    }
 #pragma unroll
-        for (int k = 0; k < kUnroll; k++) store_stream<WIDTH>(dst + threadIdx.x + k * kThreads, v[k]);
-    } else {
-        for (int64_t e = threadIdx.x; e < n; e += kThreads) store_stream<WIDTH>(dst + e, load_stream<WIDTH>(src + e));
+    for (int k = 0; k < U; k++) {
+        const int64_t e = threadIdx.x + k * kThreads;
+        if (e < m) store_stream<WIDTH>(dst + e, v[k]);
     }
 }
 
-template <int WIDTH>
+template <int WIDTH, int U>
 __device__ void copy_narrow(const CollectArgs& a, const ColTask& c, int64_t q) {
     typedef typename Elem<WIDTH>::type V;
     __shared__ int64_t s_off[kThreads];   // source element offset per window, -1 if invalid
@@ -150,9 +186,9 @@ __device__ void copy_narrow(const CollectArgs& a, const ColTask& c, int64_t q) {
     const uint32_t total = (uint32_t)nb * c.epw;
     const V* src = reinterpret_cast<const V*>(c.src);
     V* dst = reinterpret_cast<V*>(c.out) + b0 * (int64_t)c.epw;
-    V v[kUnroll];
+    V v[U];
 #pragma unroll
-    for (int k = 0; k < kUnroll; k++) {
+    for (int k = 0; k < U; k++) {
         const uint32_t e = threadIdx.x + k * kThreads;
         v[k] = zero_elem<WIDTH>();
         if (e < total) {
@@ -162,12 +198,13 @@ __device__ void copy_narrow(const CollectArgs& a, const ColTask& c, int64_t q) {
         }
     }
 #pragma unroll
-    for (int k = 0; k < kUnroll; k++) {
+    for (int k = 0; k < U; k++) {
         const uint32_t e = threadIdx.x + k * kThreads;
         if (e < total) store_stream<WIDTH>(dst + e, v[k]);
     }
 }
 
+template <int U>
 __global__ __launch_bounds__(kThreads) void collect_kernel(CollectArgs a) {
     const int64_t task = blockIdx.x;
     int j = 0;
@@ -175,13 +212,13 @@ __global__ __launch_bounds__(kThreads) void collect_kernel(CollectArgs a) {
     const ColTask& c = a.col[j];
     const int64_t q = task - c.task0;
     if (c.wide) {
-        if (c.width == 16) copy_wide<16>(a, c, q);
-        else if (c.width == 4) copy_wide<4>(a, c, q);
-        else copy_wide<1>(a, c, q);
+        if (c.width == 16) copy_wide<16, U>(a, c, q);
+        else if (c.width == 4) copy_wide<4, U>(a, c, q);
+        else copy_wide<1, U>(a, c, q);
     } else {
-        if (c.width == 16) copy_narrow<16>(a, c, q);
-        else if (c.width == 4) copy_narrow<4>(a, c, q);
-        else copy_narrow<1>(a, c, q);
+        if (c.width == 16) copy_narrow<16, U>(a, c, q);
+        else if (c.width == 4) copy_narrow<4, U>(a, c, q);
+        else copy_narrow<1, U>(a, c, q);
     }
 }
 
@@ -210,6 +247,7 @@ extern "C" int gear_collect(gear_table* h, const int64_t* d_idx, const int32_t* 
     gear::DeviceGuard guard(t->device);
     if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_collect: hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
+    const int unroll = t->residency == GEAR_HOST_PINNED ? gear::kUnrollHost : gear::kUnrollDevice;
 
     for (int j0 = 0; j0 < ncols; j0 += gear::kMaxLaunchCols) {
         gear::CollectArgs a{};
@@ -241,18 +279,17 @@ extern "C" int gear_collect(gear_table* h, const int64_t* d_idx, const int32_t* 
             if (stride % 16 == 0 && ct.W % 16 == 0 && sa % 16 == 0 && oa % 16 == 0) ct.width = 16;
             else if (stride % 4 == 0 && ct.W % 4 == 0 && sa % 4 == 0 && oa % 4 == 0) ct.width = 4;
             else ct.width = 1;
-            ct.piece = (int64_t)gear::kThreads * gear::kUnroll * ct.width;
+            ct.piece = (int64_t)gear::kThreads * unroll * ct.width;
+            ct.n = ct.W / ct.width;
             ct.task0 = tasks;
             if (ct.W >= ct.piece) {
                 ct.wide = 1;
-                ct.ppw = (ct.W + ct.piece - 1) / ct.piece;
                 ct.wpp = 1;
                 ct.epw = 0;
                 ct.magic = 0;
-                tasks += (int64_t)B * ct.ppw;
+                tasks += ((int64_t)B * ct.n + gear::kThreads * unroll - 1) / (gear::kThreads * unroll);
             } else {
                 ct.wide = 0;
-                ct.ppw = 1;
                 int64_t wpp = ct.piece / ct.W;
                 if (wpp > gear::kThreads) wpp = gear::kThreads;
                 ct.wpp = (int32_t)wpp;
@@ -262,7 +299,12 @@ extern "C" int gear_collect(gear_table* h, const int64_t* d_idx, const int32_t* 
             }
         }
         if (tasks > 0x7FFFFFFF) return fail(GEAR_E_INVAL, "gear_collect: batch too large for one launch");
-        hipLaunchKernelGGL(gear::collect_kernel, dim3((unsigned)tasks), dim3(gear::kThreads), 0, s, a);
+        if (unroll == gear::kUnrollHost)
+            hipLaunchKernelGGL(gear::collect_kernel<gear::kUnrollHost>, dim3((unsigned)tasks), dim3(gear::kThreads), 0,
+                               s, a);
+        else
+            hipLaunchKernelGGL(gear::collect_kernel<gear::kUnrollDevice>, dim3((unsigned)tasks), dim3(gear::kThreads),
+                               0, s, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return hip_fail(e, "gear_collect: launch");
     }
