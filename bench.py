@@ -34,6 +34,7 @@ METRIC = "trajectory-steps gathered/sec + gather GB/s as % of HBM / host-link pe
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
 HOST_LINK_PEAK_GBS = 63.0       # PCIe Gen5 x16 per direction: 32 GT/s * 16 * 128/130 / 8
 GATHER_SRC = os.path.join(ROOT, "paper_2310_05205_amd", "csrc", "collect.hip")
+PIPELINE_MIN_BATCH = 128 << 20  # batch bytes from which steps overlap select/update with the gather
 
 
 class HipEvents:
@@ -92,7 +93,9 @@ def parse():
                              "shard-select"])
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing (profiling runs)")
     ap.add_argument("--serial", action="store_true",
-                    help="issue every step in order on one stream (default: select/update overlap the gather)")
+                    help="issue every step in order on one stream (default for batches under 128 MiB)")
+    ap.add_argument("--pipeline", action="store_true",
+                    help="overlap select/update with the gather on two streams whatever the batch size")
     ap.add_argument("--group", type=int, default=2,
                     help="steps per cross-stream handshake when select/update overlap the gather")
     ap.add_argument("--legs", default="all", choices=["all", "headline"],
@@ -909,10 +912,14 @@ def main():
         t.set_options(opts)
     K, W = args.steps, args.warmup
     strategy = w.strategies[0]
-    # Steps of a device table with columns are pipelined over two streams;
-    # a pinned host table's gather takes milliseconds, so its steps run in
-    # order on one stream, and so does a selection-only workload.
-    pipelined = bool(w.elem_bytes) and not w.host_table and not args.serial
+    # Steps whose gather dominates (a batch of at least PIPELINE_MIN_BATCH
+    # bytes from a device table) are pipelined over two streams.  Smaller
+    # batches are launch-bound, and the cross-stream handshakes cost more
+    # than the overlap saves (DT 20-step windows: 24.2 against 12.0 us per
+    # step); a pinned host table's gather takes milliseconds; so those steps,
+    # and selection-only workloads, run in order on one stream.
+    batch = w.B * w.L * sum(w.elem_bytes)
+    pipelined = (batch >= PIPELINE_MIN_BATCH and not w.host_table and not args.serial) or args.pipeline
     r = run_steps(t, w, K, W, dev, pipelined, group=args.group, serial_too=pipelined)
     prioritized = strategy in (gear.GEAR_PRIORITIZED, gear.GEAR_TOPK)
     roof = gather_roofline(w, r["collect_ms"], args.workload) if w.elem_bytes else None
