@@ -96,7 +96,7 @@ def parse():
                     help="issue every step in order on one stream (default for batches under 128 MiB)")
     ap.add_argument("--pipeline", action="store_true",
                     help="overlap select/update with the gather on two streams whatever the batch size")
-    ap.add_argument("--group", type=int, default=2,
+    ap.add_argument("--group", type=int, default=4,
                     help="steps per cross-stream handshake when select/update overlap the gather")
     ap.add_argument("--legs", default="all", choices=["all", "headline"],
                     help="default MAT run: also measure the host-link, whole-trajectory and selection legs")
@@ -638,7 +638,36 @@ class Step:
                  "gear_update_priorities")
 
 
-def run_steps(t, w, K, W, dev, pipelined, group=2, stage_steps=50, serial_too=False):
+def concurrent_streams(dev, tries=8):
+    """Two streams from torch's pool (default priority, like every stream
+    here) whose work runs concurrently.  HIP spreads streams over a few
+    hardware queues, and two streams on one queue run one after the other:
+    pipelined steps then take as long as serial ones, which happened in about
+    one run in ten.  A pair passes if a tiny kernel on the first finishes
+    while a 1 GiB copy on the second is still running."""
+    import torch
+    big = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    small = torch.zeros(16, dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    for _ in range(tries):
+        a, b = torch.cuda.Stream(dev), torch.cuda.Stream(dev)
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(b)
+        with torch.cuda.stream(b):
+            big.mul_(1.0)
+        e[1].record(b)
+        a.wait_event(e[0])
+        with torch.cuda.stream(a):
+            small.add_(1.0)
+        e[2].record(a)
+        torch.cuda.synchronize()
+        if e[0].elapsed_time(e[2]) < 0.5 * e[0].elapsed_time(e[1]):
+            del big, small
+            return a, b
+    return None  # e.g. under a counter-collecting profiler, which serialises dispatches
+
+
+def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=False):
     """W untimed steps, then K timed ones, of workload w on table t.
 
     Serial: select, collect and update of each step on one stream, in turn
@@ -663,12 +692,18 @@ def run_steps(t, w, K, W, dev, pipelined, group=2, stage_steps=50, serial_too=Fa
     import numpy as np
     import torch
 
+    pair = concurrent_streams(dev) if pipelined else None
+    fallback = pipelined and pair is None
+    pipelined = pair is not None    # no two streams run concurrently: steps in order on one stream
     nsets = 2 * group if pipelined else 2
     step = Step(t, w, nsets, W + K, dev)
     hev = HipEvents()
-    C = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
-    side = torch.cuda.Stream(dev) if pipelined else None   # default priority, like every stream here
-    S = ctypes.c_void_p(side.cuda_stream) if pipelined else C
+    if pipelined:
+        gather_stream, side = pair
+        C, S = ctypes.c_void_p(gather_stream.cuda_stream), ctypes.c_void_p(side.cuda_stream)
+    else:
+        C = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+        S = C
     ngroups = (max(K, W) + group - 1) // group
     sel_done = [hev.create() for _ in range(ngroups)]
     col_begin = [hev.create() for _ in range(ngroups)]
@@ -724,8 +759,9 @@ def run_steps(t, w, K, W, dev, pipelined, group=2, stage_steps=50, serial_too=Fa
         col_ms = sum(hev.elapsed_ms(col_begin[g], col_done[g]) for g in range(ng)) / K
     else:
         col_ms = float(np.mean([hev.elapsed_ms(a, b) for a, b in ev]))
-    res = {"wall_s": wall, "collect_ms": col_ms, "step": step, "buffer_sets": nsets}
-    if serial_too:
+    res = {"wall_s": wall, "collect_ms": col_ms, "step": step, "buffer_sets": nsets, "pipelined": pipelined,
+           "fallback": fallback}
+    if serial_too and pipelined:
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         loop_serial(range(W, W + K), False)
@@ -921,6 +957,9 @@ def main():
     batch = w.B * w.L * sum(w.elem_bytes)
     pipelined = (batch >= PIPELINE_MIN_BATCH and not w.host_table and not args.serial) or args.pipeline
     r = run_steps(t, w, K, W, dev, pipelined, group=args.group, serial_too=pipelined)
+    if r["fallback"]:
+        print("bench.py: no two streams ran concurrently; the steps ran in order on one stream", file=sys.stderr)
+    pipelined = r["pipelined"]
     prioritized = strategy in (gear.GEAR_PRIORITIZED, gear.GEAR_TOPK)
     roof = gather_roofline(w, r["collect_ms"], args.workload) if w.elem_bytes else None
     context = torch_context(t, w, dev) if prioritized else None

@@ -33,6 +33,17 @@ constexpr int kThreads = 256;
 // host link 4% slower).
 constexpr int kUnrollDevice = 8;
 constexpr int kUnrollHost = 4;
+// A long gather from an HBM table (at least kCapRounds rounds of the
+// workgroups that fit the device) reserves kCapLds bytes of LDS per
+// workgroup that it does not use: with the kernel's own 6160 bytes that is
+// 38.9 KB, so at most 4 of its workgroups share a CU (160 KiB of LDS).  It keeps HBM as busy with 4 as with 8 (MAT batch:
+// 92.0-93.1 us with 2, 4 or 5 per CU, 92.6 us uncapped), and kernels of other
+// streams find free slots: with the next step's selection on another stream
+// the MAT step went from 103 to 99.4-99.6 us.  Short launches take every slot
+// so that they finish in one round.
+constexpr unsigned kCapLds = 32 * 1024;
+constexpr int64_t kCapRounds = 4;
+constexpr int64_t kResidentWorkgroups = 2048;  // 256 CUs x 8 workgroups of 256 threads
 constexpr int kMaxLaunchCols = 16;  // columns per launch (more take several launches)
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -299,12 +310,14 @@ extern "C" int gear_collect(gear_table* h, const int64_t* d_idx, const int32_t* 
             }
         }
         if (tasks > 0x7FFFFFFF) return fail(GEAR_E_INVAL, "gear_collect: batch too large for one launch");
-        if (unroll == gear::kUnrollHost)
+        if (unroll == gear::kUnrollHost) {
             hipLaunchKernelGGL(gear::collect_kernel<gear::kUnrollHost>, dim3((unsigned)tasks), dim3(gear::kThreads), 0,
                                s, a);
-        else
+        } else {
+            const unsigned lds = tasks >= gear::kCapRounds * gear::kResidentWorkgroups ? gear::kCapLds : 0u;
             hipLaunchKernelGGL(gear::collect_kernel<gear::kUnrollDevice>, dim3((unsigned)tasks), dim3(gear::kThreads),
-                               0, s, a);
+                               lds, s, a);
+        }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return hip_fail(e, "gear_collect: launch");
     }
