@@ -34,7 +34,14 @@
  *     caller and must stay valid until the enqueued work has completed.
  *   - A table is not thread-safe.  All calls on one table must be ordered:
  *     issue them from one host thread, on one stream, or order the streams
- *     with events.  Separate tables are independent.
+ *     with events.  Separate tables are independent.  One exception on the
+ *     device side: gear_collect reads only the columns and the caller's index
+ *     and start buffers, which selection and priority updates never write,
+ *     so its kernels may run on another stream concurrently with selection
+ *     (gear_select, the shard calls) and gear_update_priorities of the same
+ *     table, as long as the host calls still come from one thread and the
+ *     index buffers it reads are not rewritten meanwhile.  Never concurrently
+ *     with insertion, allocation or row writes, which change the columns.
  *   - HIP graph capture: gear_collect and gear_select_prioritized_noalloc
  *     keep no host-side state and may be captured and replayed.  Selection, insertion, allocation, commits and
  *     updates read and change host-side state when they are called (ring
