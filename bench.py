@@ -642,15 +642,17 @@ def concurrent_streams(dev, tries=8):
     """Two streams from torch's pool (default priority, like every stream
     here) whose work runs concurrently.  HIP spreads streams over a few
     hardware queues, and two streams on one queue run one after the other:
-    pipelined steps then take as long as serial ones, which happened in about
-    one run in ten.  A pair passes if a tiny kernel on the first finishes
-    while a 1 GiB copy on the second is still running."""
+    pipelined steps then take as long as serial ones.  A pair passes if, in
+    both directions, a tiny kernel on one finishes while a 1 GiB copy on the
+    other is still running.  Each stream first runs a tiny kernel of its
+    own: the first work on a fresh stream starts late, which failed the check
+    for pairs that overlap well (ratios 0.8-2.4 cold, 0.1 warmed), so that
+    every try could fail and the steps fell back to one stream."""
     import torch
     big = torch.empty(1 << 28, dtype=torch.float32, device=dev)
     small = torch.zeros(16, dtype=torch.float32, device=dev)
-    torch.cuda.synchronize()
-    for _ in range(tries):
-        a, b = torch.cuda.Stream(dev), torch.cuda.Stream(dev)
+
+    def finishes_inside(a, b):
         e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
         e[0].record(b)
         with torch.cuda.stream(b):
@@ -661,7 +663,16 @@ def concurrent_streams(dev, tries=8):
             small.add_(1.0)
         e[2].record(a)
         torch.cuda.synchronize()
-        if e[0].elapsed_time(e[2]) < 0.5 * e[0].elapsed_time(e[1]):
+        return e[0].elapsed_time(e[2]) < 0.5 * e[0].elapsed_time(e[1])
+
+    torch.cuda.synchronize()
+    for _ in range(tries):
+        a, b = torch.cuda.Stream(dev), torch.cuda.Stream(dev)
+        for s in (a, b):
+            with torch.cuda.stream(s):
+                small.add_(0.0)
+        torch.cuda.synchronize()
+        if finishes_inside(a, b) and finishes_inside(b, a):
             del big, small
             return a, b
     return None  # e.g. under a counter-collecting profiler, which serialises dispatches
@@ -761,6 +772,13 @@ def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=Fa
         col_ms = float(np.mean([hev.elapsed_ms(a, b) for a, b in ev]))
     res = {"wall_s": wall, "collect_ms": col_ms, "step": step, "buffer_sets": nsets, "pipelined": pipelined,
            "fallback": fallback}
+    if pipelined and ng > 1:
+        # Gather-stream time between one group's last gather and the next
+        # group's first: the handshake plus any wait for S.  About 12 us when
+        # the streams overlap; one group of selects and updates (about
+        # 100 us) when they run one after the other.
+        res["gather_stream_gap_us"] = float(np.median([hev.elapsed_ms(col_done[g - 1], col_begin[g]) * 1e3
+                                                       for g in range(1, ng)]))
     if serial_too and pipelined:
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -1006,6 +1024,7 @@ def main():
     }
     if pipelined:
         line["serial_ms_per_step"] = round(r["serial_ms_per_step"], 5)
+        line["gather_stream_gap_us_median"] = round(r["gather_stream_gap_us"], 2) if "gather_stream_gap_us" in r else None
         line["serial_value"] = round(B * L / (r["serial_ms_per_step"] * 1e-3), 1)
     if link is not None:
         line["host_link"] = link
