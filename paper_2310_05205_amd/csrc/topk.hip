@@ -321,25 +321,53 @@ __device__ __forceinline__ void threshold_range(const TopkState& st, uint64_t& l
     hi = first_priority_with_key((st.prefix + 1) << shift);
 }
 
-// Workgroup g's keys above and at the threshold, from its suffix sums of
-// every pass that ran.
-__device__ __forceinline__ void wg_counts(const uint32_t* __restrict__ local, const TopkState& st, int g,
-                                          uint32_t& gt, uint32_t& eq) {
-    if (st.flags & kAll) {
-        gt = local[(size_t)g * kBins];  // pass 0 counted every non-zero priority
-        eq = 0;
-        return;
-    }
-    gt = 0;
-    eq = 0;
+// Keys above and at the threshold of workgroups g = lane + 64 r (r < kCountRounds),
+// from their suffix sums of every pass that ran.  Every count is loaded
+// before any is used (one memory round trip): rows of passes that did not
+// run, and of workgroups past the grid, are read from valid addresses and
+// then ignored.
+constexpr int kCountRounds = kTopkMaxGrid / 64;
+static_assert(kPasses == 3, "the loads below are listed per pass");
+
+__device__ __forceinline__ void wg_counts(const uint32_t* __restrict__ local, const TopkState& st, int lane, int grid,
+                                          uint32_t gt[kCountRounds], uint32_t eq[kCountRounds]) {
+    int sel[kPasses];
 #pragma unroll
-    for (int q = 0; q < kPasses; q++) {
-        if (q >= st.passes) break;
-        const uint32_t* row = local + ((size_t)q * kTopkMaxGrid + g) * kBins;
-        const int sel = (int)(st.prefix >> (kDigit * (st.passes - 1 - q))) & (kBins - 1);
-        const uint32_t above = sel + 1 < kBins ? row[sel + 1] : 0u;
-        gt += above;
-        if (q == st.passes - 1) eq = row[sel] - above;
+    for (int q = 0; q < kPasses; q++)
+        sel[q] = q < st.passes ? (int)(st.prefix >> (kDigit * (st.passes - 1 - q))) & (kBins - 1) : 0;
+    uint32_t above[kCountRounds][kPasses], at[kCountRounds][kPasses], all[kCountRounds];
+#pragma unroll
+    for (int r = 0; r < kCountRounds; r++) {
+        const int g = lane + 64 * r < grid ? lane + 64 * r : grid - 1;
+        all[r] = local[(size_t)g * kBins];  // pass 0, bin 0: every non-zero priority of the workgroup
+#pragma unroll
+        for (int q = 0; q < kPasses; q++) {
+            const uint32_t* row = local + ((size_t)q * kTopkMaxGrid + g) * kBins;
+            above[r][q] = row[sel[q] + 1 < kBins ? sel[q] + 1 : sel[q]];
+            at[r][q] = row[sel[q]];
+        }
+    }
+    // Keeps the compiler from moving loads into the branches below.
+#pragma unroll
+    for (int r = 0; r < kCountRounds; r++)
+        asm volatile("" ::"v"(all[r]), "v"(above[r][0]), "v"(above[r][1]), "v"(above[r][2]), "v"(at[r][0]),
+                     "v"(at[r][1]), "v"(at[r][2]));
+#pragma unroll
+    for (int r = 0; r < kCountRounds; r++) {
+        gt[r] = 0;
+        eq[r] = 0;
+        if (lane + 64 * r >= grid) continue;
+        if (st.flags & kAll) {
+            gt[r] = all[r];
+            continue;
+        }
+#pragma unroll
+        for (int q = 0; q < kPasses; q++) {
+            if (q >= st.passes) break;
+            const uint32_t a = sel[q] + 1 < kBins ? above[r][q] : 0u;
+            gt[r] += a;
+            if (q == st.passes - 1) eq[r] = at[r][q] - a;
+        }
     }
 }
 
@@ -371,19 +399,19 @@ __global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(const uint32
     const int wave = threadIdx.x >> 6;
     if (wave == 0) {
         uint64_t gb = 0, eb = 0, tot = 0;
+        uint32_t gt[kCountRounds], eq[kCountRounds];
+        wg_counts(local, st, lane, grid, gt, eq);
 #pragma unroll
-        for (int r = 0; r < kTopkMaxGrid / 64; r++) {
+        for (int r = 0; r < kCountRounds; r++) {
             const int g = lane + 64 * r;
-            uint32_t gt = 0, eq = 0;
-            if (g < grid) wg_counts(local, st, g, gt, eq);
-            tot += gt;
+            tot += gt[r];
             if (g < (int)blockIdx.x) {
-                gb += gt;
-                eb += eq;
+                gb += gt[r];
+                eb += eq[r];
             }
             if (g == (int)blockIdx.x) {
-                s_base[3] = gt;
-                s_base[4] = eq;
+                s_base[3] = gt[r];
+                s_base[4] = eq[r];
             }
         }
         gb = wave_sum(gb);
@@ -473,20 +501,31 @@ __device__ __forceinline__ int selected(const TopkState& st, int32_t K) {
 // into rank[i].
 constexpr int kRankKeys = 256;
 constexpr int kRankBlock = kTopkRankBlock;
+static_assert(kRankBlock == 2 * kRankKeys, "each thread stages two keys of the block");
 
 __global__ __launch_bounds__(kRankKeys) void topk_rank_kernel(const uint64_t* __restrict__ keys,
                                                               const TopkState* __restrict__ state, int32_t K,
                                                               uint32_t* __restrict__ rank) {
     __shared__ ulonglong2 blk[kRankBlock / 2];
-    const int n = selected(*state, K);
     const int i0 = blockIdx.x * kRankKeys;
     const int j0 = blockIdx.y * kRankBlock;
-    if (i0 >= n || j0 >= n) return;
-    uint64_t* b64 = reinterpret_cast<uint64_t*>(blk);
-    for (int jj = threadIdx.x; jj < kRankBlock; jj += kRankKeys)
-        b64[jj] = j0 + jj < n ? keys[j0 + jj] : 0ull;  // 0: below every key (p >= 1)
     const int i = i0 + (int)threadIdx.x;
-    const uint64_t mine = i < n ? keys[i] : ~0ull;
+    // The state and every key this thread needs are loaded together (one
+    // memory round trip), from indices clamped into the K-entry buffer;
+    // entries at or past the selected count are then replaced.
+    const int ja = j0 + (int)threadIdx.x, jb = ja + kRankKeys;
+    const uint64_t ka = keys[ja < K ? ja : K - 1];
+    const uint64_t kb = keys[jb < K ? jb : K - 1];
+    const uint64_t km = keys[i < K ? i : K - 1];
+    const int n = selected(*state, K);
+    if (i0 >= n || j0 >= n) {
+        asm volatile("" ::"v"(ka), "v"(kb), "v"(km));  // no loads left in flight at the end
+        return;
+    }
+    uint64_t* b64 = reinterpret_cast<uint64_t*>(blk);
+    b64[threadIdx.x] = ja < n ? ka : 0ull;  // 0: below every key (p >= 1)
+    b64[threadIdx.x + kRankKeys] = jb < n ? kb : 0ull;
+    const uint64_t mine = i < n ? km : ~0ull;
     __syncthreads();
     uint32_t c0 = 0, c1 = 0;
 #pragma unroll 16
@@ -502,19 +541,26 @@ __global__ void topk_emit_kernel(const uint64_t* __restrict__ keys, const uint32
                                  const TopkState* __restrict__ state, int32_t K, uint64_t span, uint64_t seed,
                                  int64_t* __restrict__ idx, int32_t* __restrict__ start, float* __restrict__ w,
                                  uint32_t* status, uint32_t* __restrict__ hist) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    // The state, this thread's rank and its key are loaded together, from
+    // an index clamped into the K-entry buffers.
+    const int64_t tc = t < K ? t : K - 1;
+    const uint32_t b = rank[tc];  // for t < n: a permutation of 0 .. n-1
+    const uint64_t key = keys[tc];
     const TopkState st = *state;
     const int n = selected(st, K);
-    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (t < kPasses * kBins) hist[t] = 0u;  // every digit pass of this call is done
     if (t == 0 && (st.flags & kInconsistent)) atomicOr(status, GEAR_STATUS_INTERNAL);
-    if (t >= K) return;
+    if (t >= K) {
+        asm volatile("" ::"v"(b), "v"(key));  // no loads left in flight at the end
+        return;
+    }
     if (t < n) {
-        const uint32_t b = rank[t];  // a permutation of 0 .. n-1
         if (b >= (uint32_t)n) {
             atomicOr(status, GEAR_STATUS_INTERNAL);
             return;
         }
-        idx[b] = (int64_t)(0xFFFFFFFFu - (uint32_t)keys[t]);
+        idx[b] = (int64_t)(0xFFFFFFFFu - (uint32_t)key);
         start[b] = (int32_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b + 1), span);
         if (w) w[b] = 1.0f;
     } else {
