@@ -42,7 +42,18 @@ struct Levels {
     uint64_t* level[kMaxLevels];   // level 0: tile sums; level l: sums of 256^l tiles
     int64_t size[kMaxLevels];
     int nlevels;
+    // The top level again (level[nlevels - 1]), so that a search reads it
+    // without first waiting for nlevels.
+    const uint64_t* top;
+    int64_t top_size;
 };
+
+// Sets the top-level copy of a search's levels.
+inline Levels with_top(Levels lv) {
+    lv.top = lv.level[lv.nlevels - 1];
+    lv.top_size = lv.size[lv.nlevels - 1];
+    return lv;
+}
 
 // Inclusive prefix of 256 values held four per lane (lane l holds values
 // 4l..4l+3): c0..c3 receive the prefix at this lane's four positions.
@@ -184,7 +195,7 @@ __global__ __launch_bounds__(256) void search_kernel(const uint32_t* __restrict_
 
     // The top level is the same for every draw: its prefix and total once.
     uint64_t t0, t1, t2, t3, tc0, tc1, tc2, tc3;
-    load4_u64(lv.level[top], lv.size[top], lane * 4, t0, t1, t2, t3);
+    load4_u64(lv.top, lv.top_size, lane * 4, t0, t1, t2, t3);
     wave_prefix4(t0, t1, t2, t3, tc0, tc1, tc2, tc3);
     const uint64_t S = read_lane(tc3, 63);
     // Draws are numbers in [0, S_all); this table owns [P, P + S).
@@ -269,12 +280,26 @@ __global__ __launch_bounds__(256) void is_weights_kernel(int32_t B, double beta,
                                                          int search_grid, float* __restrict__ w) {
     __shared__ uint32_t s_min[4];
     const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const uint32_t pb = b < B ? reinterpret_cast<const uint32_t*>(w)[b] : 0u;
-    // Eight minima per thread are loaded before any is compared, so one
-    // memory round trip covers the search's largest grid.
+    // This draw's priority and the first eight minima per thread are loaded
+    // together, from indices clamped into their buffers, before any is used:
+    // one memory round trip covers the search's largest grid.
     constexpr int kMinPerThread = 8;
+    const uint32_t pb_raw = reinterpret_cast<const uint32_t*>(w)[b < B ? b : B - 1];
+    uint32_t v0[kMinPerThread];
+#pragma unroll
+    for (int u = 0; u < kMinPerThread; u++) {
+        const int k = (int)threadIdx.x + u * (int)blockDim.x;
+        v0[u] = wg_min[k < search_grid ? k : 0];
+    }
+    const uint32_t pb = b < B ? pb_raw : 0u;
     uint32_t m = 0xFFFFFFFFu;
-    for (int k0 = threadIdx.x; k0 < search_grid; k0 += blockDim.x * kMinPerThread) {
+#pragma unroll
+    for (int u = 0; u < kMinPerThread; u++) {
+        const int k = (int)threadIdx.x + u * (int)blockDim.x;
+        m = (k < search_grid && v0[u] < m) ? v0[u] : m;
+    }
+    // Grids larger than blockDim * kMinPerThread (the table's chunk minima).
+    for (int k0 = threadIdx.x + blockDim.x * kMinPerThread; k0 < search_grid; k0 += blockDim.x * kMinPerThread) {
         uint32_t v[kMinPerThread];
 #pragma unroll
         for (int u = 0; u < kMinPerThread; u++) {
@@ -430,7 +455,7 @@ Levels tree(const Table& t) {
         lv.level[l] = l == 0 ? t.tile_sums : t.upper[t.tree_parity][l];
         lv.size[l] = t.level_size[l];
     }
-    return lv;
+    return with_top(lv);
 }
 
 Levels upper_copy(const Table& t, int parity) {
@@ -686,8 +711,8 @@ extern "C" int gear_select_prioritized_noalloc(const uint32_t* d_priority, int64
         what = "gear_select_prioritized_noalloc: search launch";
         Shard sh{};
         sh.G = 1;
-        hipLaunchKernelGGL(search_kernel<false>, dim3(grid), dim3(256), 0, s, d_priority, N, lv, B, span, seed,
-                           d_weights ? 1 : 0, sh, wg_min, status, d_idx, d_start,
+        hipLaunchKernelGGL(search_kernel<false>, dim3(grid), dim3(256), 0, s, d_priority, N, with_top(lv), B, span,
+                           seed, d_weights ? 1 : 0, sh, wg_min, status, d_idx, d_start,
                            reinterpret_cast<uint32_t*>(d_weights));
         e = hipGetLastError();
     }

@@ -82,20 +82,36 @@ __global__ __launch_bounds__(kHashThreads) void scatter_lds_kernel(const int64_t
         slot[k] = b < B ? idx[b] : -1;
         val[k] = b < B ? newp[b] : 0u;
     }
-    // Draws of this workgroup's partition.  Their old priorities are read
-    // now, overlapping the hash phase: only the winning draw of a slot
-    // writes it, and only after the barrier below.
+    // Draws of this workgroup's partition.  Their committed flags and old
+    // priorities are read now, overlapping the hash phase, all issued
+    // before any is used (from slot 0 for an invalid draw, then ignored):
+    // only the winning draw of a slot writes it, and only after the barrier
+    // below.  Reading another partition's slot that its workgroup may be
+    // writing is harmless, since the value is discarded.
     bool mine[kPerThread];
     uint32_t old[kPerThread];
+    uint32_t flag[kPerThread];
     bool bad = false;
 #pragma unroll
     for (int k = 0; k < kPerThread; k++) {
         const int b = threadIdx.x + k * kHashThreads;
         const bool valid = b < B && slot[k] >= 0 && slot[k] < live;
+        const int64_t s = valid ? slot[k] : 0;
+        flag[k] = committed != nullptr ? committed[s] : 1u;
+        old[k] = tree.maintain ? prio[s] : 0u;
+    }
+    static_assert(kPerThread == 8, "the values below are listed per draw");
+    // Keeps the compiler from waiting on each load before issuing the next.
+    asm volatile("" ::"v"(flag[0]), "v"(flag[1]), "v"(flag[2]), "v"(flag[3]), "v"(flag[4]), "v"(flag[5]),
+                 "v"(flag[6]), "v"(flag[7]), "v"(old[0]), "v"(old[1]), "v"(old[2]), "v"(old[3]), "v"(old[4]),
+                 "v"(old[5]), "v"(old[6]), "v"(old[7]));
+#pragma unroll
+    for (int k = 0; k < kPerThread; k++) {
+        const int b = threadIdx.x + k * kHashThreads;
+        const bool valid = b < B && slot[k] >= 0 && slot[k] < live;
         if (b < B && !valid && blockIdx.x == 0) bad = true;
-        mine[k] = valid && (((uint32_t)slot[k] * 0x85EBCA6Bu) >> (32 - kPartBits)) == blockIdx.x &&
-                  (committed == nullptr || committed[slot[k]] != 0);
-        old[k] = (tree.maintain && mine[k]) ? prio[slot[k]] : 0u;
+        mine[k] = valid && (((uint32_t)slot[k] * 0x85EBCA6Bu) >> (32 - kPartBits)) == blockIdx.x && flag[k] != 0;
+        if (!mine[k]) old[k] = 0u;
     }
     __syncthreads();
     int pos[kPerThread];
