@@ -43,8 +43,9 @@
  *     index buffers it reads are not rewritten meanwhile.  Never concurrently
  *     with insertion, allocation or row writes, which change the columns.
  *   - HIP graph capture: gear_collect and gear_select_prioritized_noalloc
- *     keep no host-side state and may be captured and replayed.  Selection, insertion, allocation, commits and
- *     updates read and change host-side state when they are called (ring
+ *     keep no host-side state and may be captured and replayed.  Selection,
+ *     insertion, allocation, commits and updates read and change host-side
+ *     state when they are called (ring
  *     counters, whether the sum tree is current, which copy of its upper
  *     levels is live), so a replayed capture would repeat stale decisions:
  *     call them directly.
