@@ -26,21 +26,30 @@ namespace gear {
 namespace {
 
 constexpr int kThreads = 256;
-// Elements in flight per thread.  HBM tables: 8, pieces of 32 KiB at 16-byte
-// elements (a 102 MB launch of whole DT-shaped trajectories then runs in
-// about one round of resident workgroups: 20.1 against 21.3 us with 16 KiB
-// pieces).  Pinned host tables: 4, pieces of 16 KiB (32 KiB pieces read the
-// host link 4% slower).
-constexpr int kUnrollDevice = 8;
+// Elements in flight per thread (U), so a piece is kThreads * U elements.
+// HBM tables: 8 (32 KiB pieces at 16-byte elements) for batches of at least
+// kLargeBatch bytes, 2 (8 KiB) below.  Measured on gfx950 in one process,
+// each variant alternating on the same table and buffers: the DT-shaped
+// whole trajectories (51 MB) 20.6-20.7 us with 2 against 20.9-21.2 with 4
+// and 21.5-22.1 with 8; 8.7 MB and 2 MB batches 4.8 and 4.5 us with 2
+// against 5.5 and 5.1 with 8.  The MAT batch (278 MB) took 103.6 us with 2
+// and 94.6 with 4 against 96.0 with 8 back to back, but with the next
+// steps' selection running beside it on another stream, as in the replay
+// loop, 4 was the slower (gather 94.1 against 92.7 us, step 97.9 against
+// 97.2 over 100 steps).  Pinned host tables: 4 (8 was 4% slower over the host
+// link; 2 no faster).
+constexpr int kUnrollLarge = 8;
+constexpr int kUnrollSmall = 2;
+constexpr int64_t kLargeBatch = 128ll << 20;
 constexpr int kUnrollHost = 4;
 // A long gather from an HBM table (at least kCapRounds rounds of the
 // workgroups that fit the device) reserves kCapLds bytes of LDS per
-// workgroup that it does not use: with the kernel's own 6160 bytes that is
-// 38.9 KB, so at most 4 of its workgroups share a CU (160 KiB of LDS).  It keeps HBM as busy with 4 as with 8 (MAT batch:
-// 92.0-93.1 us with 2, 4 or 5 per CU, 92.6 us uncapped), and kernels of other
-// streams find free slots: with the next step's selection on another stream
-// the MAT step went from 103 to 99.4-99.6 us.  Short launches take every slot
-// so that they finish in one round.
+// workgroup that it does not use: with the kernel's own LDS that is about
+// 39 KB, so at most 4 of its workgroups share a CU (160 KiB of LDS).  It
+// keeps HBM as busy with 4 as with 8 (MAT batch: 92.0-93.1 us with 2, 4 or 5
+// per CU, 92.6 us uncapped), and kernels of other streams find free slots:
+// with the next step's selection on another stream the MAT step went from
+// 103 to 99.4-99.6 us.  Shorter launches take every slot.
 constexpr unsigned kCapLds = 32 * 1024;
 constexpr int64_t kCapRounds = 4;
 constexpr int64_t kResidentWorkgroups = 2048;  // 256 CUs x 8 workgroups of 256 threads
@@ -113,6 +122,20 @@ __device__ inline typename Elem<WIDTH>::type zero_elem() {
     return typename Elem<WIDTH>::type(0);
 }
 
+// Element k (< U) of this thread within its piece of kThreads * U elements.
+// Each wave owns 64 * U consecutive elements and its k-th load covers the
+// k-th 64 of them, so every wave reads and writes one contiguous run instead
+// of the four waves interleaving every 64 elements.  On gfx950 a 278 MB copy
+// with 4 KiB per wave took 88.5-88.9 us, against 96.4-96.9 us with 32 KiB
+// pieces interleaved that way.  In the gather it is worth less: the MAT
+// batch with 8 elements per thread 91.1-96.0 us against 91.2-96.7
+// interleaved (two machines), and no difference next to another stream's
+// selection; the DT-shaped batch with 2, 20.6 against 20.9 us.
+template <int U>
+__device__ __forceinline__ int64_t lane_elem(int k) {
+    return (int64_t)(threadIdx.x >> 6) * (64 * U) + k * 64 + (threadIdx.x & 63);
+}
+
 // Source byte offset of window b's first step; kNoWindow for index -1 (a
 // draw with no trajectory: a missing TopK entry, a draw another shard
 // owns), kBadWindow for an index or start out of range.  Both read as zeros.
@@ -154,18 +177,18 @@ __device__ void copy_wide(const CollectArgs& a, const ColTask& c, int64_t q) {
         // Every element valid: the loads go out unconditionally, all in flight.
 #pragma unroll
         for (int k = 0; k < U; k++) {
-            const int64_t r = r0 + threadIdx.x + k * kThreads;
+            const int64_t r = r0 + lane_elem<U>(k);
             v[k] = load_stream<WIDTH>(src + (r < c.n ? b0 : b1) + r);
         }
 #pragma unroll
-        for (int k = 0; k < U; k++) store_stream<WIDTH>(dst + threadIdx.x + k * kThreads, v[k]);
+        for (int k = 0; k < U; k++) store_stream<WIDTH>(dst + lane_elem<U>(k), v[k]);
         return;
     }
     // The batch's last piece, or a piece touching a missing or invalid
     // window (whose elements are zero).
 #pragma unroll
     for (int k = 0; k < U; k++) {
-        const int64_t e = threadIdx.x + k * kThreads;
+        const int64_t e = lane_elem<U>(k);
         const int64_t r = r0 + e;
         const bool second = r >= c.n;
         v[k] = zero_elem<WIDTH>();
@@ -173,7 +196,7 @@ __device__ void copy_wide(const CollectArgs& a, const ColTask& c, int64_t q) {
     }
 #pragma unroll
     for (int k = 0; k < U; k++) {
-        const int64_t e = threadIdx.x + k * kThreads;
+        const int64_t e = lane_elem<U>(k);
         if (e < m) store_stream<WIDTH>(dst + e, v[k]);
     }
 }
@@ -200,7 +223,7 @@ __device__ void copy_narrow(const CollectArgs& a, const ColTask& c, int64_t q) {
     V v[U];
 #pragma unroll
     for (int k = 0; k < U; k++) {
-        const uint32_t e = threadIdx.x + k * kThreads;
+        const uint32_t e = (uint32_t)lane_elem<U>(k);
         v[k] = zero_elem<WIDTH>();
         if (e < total) {
             const uint32_t w = c.epw == 1 ? e : __umulhi(e, c.magic);
@@ -210,7 +233,7 @@ __device__ void copy_narrow(const CollectArgs& a, const ColTask& c, int64_t q) {
     }
 #pragma unroll
     for (int k = 0; k < U; k++) {
-        const uint32_t e = threadIdx.x + k * kThreads;
+        const uint32_t e = (uint32_t)lane_elem<U>(k);
         if (e < total) store_stream<WIDTH>(dst + e, v[k]);
     }
 }
@@ -258,7 +281,11 @@ extern "C" int gear_collect(gear_table* h, const int64_t* d_idx, const int32_t* 
     gear::DeviceGuard guard(t->device);
     if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_collect: hipSetDevice");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const int unroll = t->residency == GEAR_HOST_PINNED ? gear::kUnrollHost : gear::kUnrollDevice;
+    const bool pinned = t->residency == GEAR_HOST_PINNED;
+    int64_t batch_bytes = 0;
+    for (int j = 0; j < ncols; j++) batch_bytes += (int64_t)B * L * t->elem_bytes[col_ids ? col_ids[j] : j];
+    const int unroll = pinned ? gear::kUnrollHost
+                              : batch_bytes >= gear::kLargeBatch ? gear::kUnrollLarge : gear::kUnrollSmall;
 
     for (int j0 = 0; j0 < ncols; j0 += gear::kMaxLaunchCols) {
         gear::CollectArgs a{};
@@ -310,14 +337,16 @@ extern "C" int gear_collect(gear_table* h, const int64_t* d_idx, const int32_t* 
             }
         }
         if (tasks > 0x7FFFFFFF) return fail(GEAR_E_INVAL, "gear_collect: batch too large for one launch");
-        if (unroll == gear::kUnrollHost) {
-            hipLaunchKernelGGL(gear::collect_kernel<gear::kUnrollHost>, dim3((unsigned)tasks), dim3(gear::kThreads), 0,
-                               s, a);
-        } else {
-            const unsigned lds = tasks >= gear::kCapRounds * gear::kResidentWorkgroups ? gear::kCapLds : 0u;
-            hipLaunchKernelGGL(gear::collect_kernel<gear::kUnrollDevice>, dim3((unsigned)tasks), dim3(gear::kThreads),
+        const unsigned lds = !pinned && tasks >= gear::kCapRounds * gear::kResidentWorkgroups ? gear::kCapLds : 0u;
+        if (unroll == gear::kUnrollLarge)
+            hipLaunchKernelGGL(gear::collect_kernel<gear::kUnrollLarge>, dim3((unsigned)tasks), dim3(gear::kThreads),
                                lds, s, a);
-        }
+        else if (unroll == gear::kUnrollHost)
+            hipLaunchKernelGGL(gear::collect_kernel<gear::kUnrollHost>, dim3((unsigned)tasks), dim3(gear::kThreads),
+                               lds, s, a);
+        else
+            hipLaunchKernelGGL(gear::collect_kernel<gear::kUnrollSmall>, dim3((unsigned)tasks), dim3(gear::kThreads),
+                               lds, s, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return hip_fail(e, "gear_collect: launch");
     }
