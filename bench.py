@@ -589,7 +589,7 @@ class Step:
     starts, weights and one batch buffer per column) are used in turn, so
     no batch line is still cached from the step before."""
 
-    def __init__(self, t, w, nsets, iters, dev):
+    def __init__(self, t, w, nsets, iters, dev, options=0):
         import numpy as np
         import torch
 
@@ -598,6 +598,7 @@ class Step:
 
         self.gear, self.lib = gear, gear.lib()
         self.tab = ctypes.c_void_p(t.handle)
+        self.options = options
         self.B, self.L = w.B, w.L
         self.strategy = w.strategies[0]
         self.updates = self.strategy in (gear.GEAR_PRIORITIZED, gear.GEAR_TOPK)
@@ -636,6 +637,11 @@ class Step:
     def update(self, it, k, sh):
         self._ok(self.lib.gear_update_priorities(self.tab, self.ip[k], self.np_[it], self.B, sh),
                  "gear_update_priorities")
+
+    def share_cus(self, on):
+        """Gathers enqueued from now on leave room for the other stream (on) or not."""
+        opts = self.options | (self.gear.GEAR_OPT_GATHER_SHARE_CU if on else 0)
+        self._ok(self.lib.gear_table_set_options(self.tab, ctypes.c_uint32(opts)), "gear_table_set_options")
 
 
 def concurrent_streams(dev, tries=8):
@@ -678,16 +684,56 @@ def concurrent_streams(dev, tries=8):
     return None  # e.g. under a counter-collecting profiler, which serialises dispatches
 
 
-def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=False):
+# Sizes of a pipeline's first groups.  The gather stream waits for the first
+# group's selections and updates before it can start, about 23 us per step
+# on an idle GPU, so the pipeline starts with one step, then two, then
+# `group` per handshake.  Beside gathers that hold 4 workgroups per CU the
+# selection stream is no faster than the gathers, and it would then fall
+# behind a growing group; during the ramp the gathers therefore run with
+# GEAR_OPT_GATHER_SHARE_CU, which halves the selection chain's time beside
+# them.  MAT steps, one table, configurations alternated in one process:
+# 100.1-100.5 against 102.1-102.4 us per step over 20 steps, and 96.6-96.9
+# against 97.0-97.4 over 100.  With the option in every group the 20-step
+# figure is the same, and the 100-step one up to 0.7 us worse.
+RAMP = (1, 2)
+
+
+def pipeline_groups(n, group, ramp=RAMP):
+    """Positions 0..n-1 split into handshake groups: the ramp's sizes (at most
+    `group` each), then `group` steps per group."""
+    sizes = [min(r, group) for r in ramp]
+    out, j, g = [], 0, 0
+    while j < n:
+        size = sizes[g] if g < len(sizes) else group
+        out.append(list(range(j, min(n, j + size))))
+        j += size
+        g += 1
+    return out
+
+
+def set_reuse_waits(groups, nsets):
+    """For each group, the earlier groups whose gathers the selection stream
+    must see finished before it writes the group's buffer sets (a step at
+    position j uses set j % nsets)."""
+    last, waits = {}, []
+    for g, js in enumerate(groups):
+        waits.append(sorted({last[j % nsets] for j in js if j % nsets in last}))
+        for j in js:
+            last[j % nsets] = g
+    return waits
+
+
+def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=False, options=0):
     """W untimed steps, then K timed ones, of workload w on table t.
 
     Serial: select, collect and update of each step on one stream, in turn
     over two buffer sets.
     Pipelined: select and update on a second stream S, collect on the
-    current stream C, in groups of `group` steps over 2*group buffer sets.
-    S issues the selects and updates of a group, then one event; C waits for
-    that event once and runs the group's gathers, then records one event,
-    which S waits for before it reuses those buffer sets two groups later.
+    current stream C, in groups over 2*group buffer sets: one step, two,
+    then `group` steps per group (RAMP).  S issues the selects and updates
+    of a group, then one event; C waits for that event once and runs the
+    group's gathers, then records one event, which S waits for before it
+    reuses those buffer sets in a later group.
     Every select still follows the previous step's update on S, so each step
     draws exactly what the serial order draws; the selects and updates of
     the next group overlap this group's gathers.  A cross-stream wait and a
@@ -707,7 +753,7 @@ def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=Fa
     fallback = pipelined and pair is None
     pipelined = pair is not None    # no two streams run concurrently: steps in order on one stream
     nsets = 2 * group if pipelined else 2
-    step = Step(t, w, nsets, W + K, dev)
+    step = Step(t, w, nsets, W + K, dev, options)
     hev = HipEvents()
     if pipelined:
         gather_stream, side = pair
@@ -715,7 +761,7 @@ def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=Fa
     else:
         C = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
         S = C
-    ngroups = (max(K, W) + group - 1) // group
+    ngroups = len(pipeline_groups(max(K, W), group))
     sel_done = [hev.create() for _ in range(ngroups)]
     col_begin = [hev.create() for _ in range(ngroups)]
     col_done = [hev.create() for _ in range(ngroups)]
@@ -736,10 +782,10 @@ def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=Fa
 
     def loop_pipe(its):
         its = list(its)
-        for g in range(0, (len(its) + group - 1) // group):
-            js = range(g * group, min(len(its), (g + 1) * group))
-            if g >= 2:
-                hev.wait(S.value, col_done[g - 2])
+        groups = pipeline_groups(len(its), group)
+        for g, (js, waits) in enumerate(zip(groups, set_reuse_waits(groups, nsets))):
+            for p in waits:
+                hev.wait(S.value, col_done[p])
             for j in js:
                 step.select(its[j], j % nsets, S)
                 if step.updates:
@@ -747,10 +793,12 @@ def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=Fa
             hev.record(sel_done[g], S.value)
             hev.wait(C.value, sel_done[g])
             hev.record(col_begin[g], C.value)
+            step.share_cus(g < len(RAMP))
             for j in js:
                 step.collect(j % nsets, C)
             hev.record(col_done[g], C.value)
-        return (len(its) + group - 1) // group
+        step.share_cus(False)
+        return len(groups)
 
     if pipelined:
         loop_pipe(range(W))
@@ -974,7 +1022,7 @@ def main():
     # and selection-only workloads, run in order on one stream.
     batch = w.B * w.L * sum(w.elem_bytes)
     pipelined = (batch >= PIPELINE_MIN_BATCH and not w.host_table and not args.serial) or args.pipeline
-    r = run_steps(t, w, K, W, dev, pipelined, group=args.group, serial_too=pipelined)
+    r = run_steps(t, w, K, W, dev, pipelined, group=args.group, serial_too=pipelined, options=opts)
     if r["fallback"]:
         print("bench.py: no two streams ran concurrently; the steps ran in order on one stream", file=sys.stderr)
     pipelined = r["pipelined"]
@@ -1011,7 +1059,8 @@ def main():
                    "is_normalisation": "table minimum" if args.global_min else "batch minimum",
                    "steps_issued": "two streams, select/update overlapping the gather" if pipelined
                    else "one stream, in order", "batch_buffer_sets": r["buffer_sets"],
-                   "steps_per_handshake": args.group if pipelined else None},
+                   "steps_per_handshake": args.group if pipelined else None,
+                   "first_groups": [min(x, args.group) for x in RAMP] if pipelined else None},
         "roofline": roof,
         "cpu_baseline": cpu,
         "stages_ms": {"select": round(sm["select"], 5),

@@ -97,6 +97,11 @@ extern "C" {
                                          non-zero priority of the whole table, not of the
                                          batch (every select after a change rescans; updates
                                          then do not maintain the tree) */
+#define GEAR_OPT_GATHER_SHARE_CU  4u  /* long gathers from an HBM table hold at most 2
+                                         workgroups per CU instead of 4, so that kernels
+                                         on other streams start sooner beside them; the
+                                         gather itself runs about 1% slower.  Results
+                                         are unchanged. */
 
 /* Limits. */
 #define GEAR_MAX_CAPACITY  (1ll << 30)  /* keeps every priority total below 2^62 */

@@ -50,7 +50,13 @@ constexpr int kUnrollHost = 4;
 // per CU, 92.6 us uncapped), and kernels of other streams find free slots:
 // with the next step's selection on another stream the MAT step went from
 // 103 to 99.4-99.6 us.  Shorter launches take every slot.
+// GEAR_OPT_GATHER_SHARE_CU reserves kShareLds instead (about 71 KB with the
+// kernel's own LDS, so 2 per CU).  Beside such a gather the MAT selection and
+// update take about half as long as beside one with 4 per CU, while the
+// gather takes 1-1.5 us longer: worth it only while another stream has to
+// catch up, as at the start of a pipeline.
 constexpr unsigned kCapLds = 32 * 1024;
+constexpr unsigned kShareLds = 64 * 1024;
 constexpr int64_t kCapRounds = 4;
 constexpr int64_t kResidentWorkgroups = 2048;  // 256 CUs x 8 workgroups of 256 threads
 constexpr int kMaxLaunchCols = 16;  // columns per launch (more take several launches)
@@ -337,7 +343,8 @@ extern "C" int gear_collect(gear_table* h, const int64_t* d_idx, const int32_t* 
             }
         }
         if (tasks > 0x7FFFFFFF) return fail(GEAR_E_INVAL, "gear_collect: batch too large for one launch");
-        const unsigned lds = !pinned && tasks >= gear::kCapRounds * gear::kResidentWorkgroups ? gear::kCapLds : 0u;
+        const unsigned cap = (t->options & GEAR_OPT_GATHER_SHARE_CU) ? gear::kShareLds : gear::kCapLds;
+        const unsigned lds = !pinned && tasks >= gear::kCapRounds * gear::kResidentWorkgroups ? cap : 0u;
         if (unroll == gear::kUnrollLarge)
             hipLaunchKernelGGL(gear::collect_kernel<gear::kUnrollLarge>, dim3((unsigned)tasks), dim3(gear::kThreads),
                                lds, s, a);

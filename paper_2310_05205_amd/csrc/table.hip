@@ -372,7 +372,7 @@ extern "C" int gear_insert(gear_table* h, int64_t n, const void* const* col_src,
 
 extern "C" int gear_table_set_options(gear_table* h, uint32_t options) {
     if (h == nullptr) return fail(GEAR_E_INVAL, "gear_table_set_options: table is NULL");
-    if (options & ~(GEAR_OPT_INCREMENTAL_TREE | GEAR_OPT_IS_GLOBAL_MIN))
+    if (options & ~(GEAR_OPT_INCREMENTAL_TREE | GEAR_OPT_IS_GLOBAL_MIN | GEAR_OPT_GATHER_SHARE_CU))
         return fail(GEAR_E_INVAL, "gear_table_set_options: unknown option bits");
     Table* t = reinterpret_cast<Table*>(h);
     // Chunk minima are exact only right after a scan: switching the global

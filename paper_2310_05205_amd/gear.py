@@ -38,6 +38,7 @@ GEAR_NOALLOC_MAX_N = 1 << 24
 GEAR_NOALLOC_SCRATCH_BYTES = 536832
 GEAR_OPT_INCREMENTAL_TREE = 1
 GEAR_OPT_IS_GLOBAL_MIN = 2
+GEAR_OPT_GATHER_SHARE_CU = 4
 GEAR_DTYPE_U8, GEAR_DTYPE_I8, GEAR_DTYPE_U16, GEAR_DTYPE_I16, GEAR_DTYPE_F16, GEAR_DTYPE_BF16 = 0, 1, 2, 3, 4, 5
 GEAR_DTYPE_U32, GEAR_DTYPE_I32, GEAR_DTYPE_F32, GEAR_DTYPE_U64, GEAR_DTYPE_I64, GEAR_DTYPE_F64 = 6, 7, 8, 9, 10, 11
 GEAR_MAX_NAME = 63

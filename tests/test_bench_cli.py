@@ -35,3 +35,39 @@ def test_traffic_comes_from_a_summary_of_the_current_source(tmp_path, monkeypatc
     assert bench.profiled_traffic("other_kernel", "mat") is None
     assert bench.profiled_traffic("collect_kernel", "dt") is None
 
+
+
+def test_pipeline_groups_ramp_then_fixed_size():
+    assert bench.pipeline_groups(0, 4) == []
+    assert [len(g) for g in bench.pipeline_groups(20, 4)] == [1, 2, 4, 4, 4, 4, 1]
+    assert [len(g) for g in bench.pipeline_groups(5, 4)] == [1, 2, 2]
+    assert [len(g) for g in bench.pipeline_groups(6, 1)] == [1] * 6
+    for group in range(1, 9):
+        for n in range(0, 41):
+            gl = bench.pipeline_groups(n, group)
+            assert [j for g in gl for j in g] == list(range(n))
+            assert all(1 <= len(g) <= group for g in gl)
+
+
+def test_buffer_sets_are_not_rewritten_before_their_gathers_end():
+    """The selection stream writes a step's set only after the gather stream
+    has finished every earlier group that used that set (gathers run in
+    order, so waiting for a group covers the groups before it).  With
+    2*group sets it never waits for the group just before, which the gather
+    stream is still running while the next group is selected."""
+    for group in range(1, 9):
+        nsets = 2 * group
+        for n in range(0, 60):
+            gl = bench.pipeline_groups(n, group)
+            waits = bench.set_reuse_waits(gl, nsets)
+            assert len(waits) == len(gl)
+            seen = -1      # latest group the selection stream has waited for
+            last = {}
+            for g, (js, ws) in enumerate(zip(gl, waits)):
+                assert len({j % nsets for j in js}) == len(js)
+                seen = max([seen] + ws)
+                for j in js:
+                    assert last.get(j % nsets, -1) <= seen
+                assert g - 1 not in ws
+                for j in js:
+                    last[j % nsets] = g

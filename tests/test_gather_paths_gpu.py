@@ -51,3 +51,33 @@ def test_both_sides_of_the_large_batch_size(L):
         assert t.sync() == 0
     finally:
         t.close()
+
+
+# 4096 whole 64-step windows of 1 KiB steps make 8192 workgroups of the
+# 1 KiB column, enough for a gather that caps its workgroups per CU.
+# GEAR_OPT_GATHER_SHARE_CU only lowers that cap: the bytes are the same.
+def test_share_option_moves_the_same_bytes():
+    N, T, L, eb = 4096, 64, 64, [1024, 4]
+    g = torch.Generator(device=cuda()).manual_seed(9)
+    t = gear.Table(eb, N, T, gear.GEAR_DEVICE, 0)
+    try:
+        rows = [torch.randint(0, 256, (N, T * e), dtype=torch.uint8, device=cuda(), generator=g) for e in eb]
+        t.insert(rows, torch.ones(N, dtype=torch.int32, device=cuda()))
+        idx, start, _ = t.select(gear.GEAR_UNIFORM, N, L, 78)
+        say("share option: %d windows of %d bytes" % (N, L * sum(eb)))
+        plain = t.collect(idx, start, L)
+        t.set_options(gear.GEAR_OPT_GATHER_SHARE_CU)
+        shared = t.collect(idx, start, L)
+        t.set_options(0)
+        again = t.collect(idx, start, L)
+        ref = _reference(t, idx, start, L)
+        torch.cuda.synchronize()
+        for c in range(len(eb)):
+            assert torch.equal(plain[c], ref[c]), "column %d" % c
+            assert torch.equal(shared[c], ref[c]), "column %d, shared" % c
+            assert torch.equal(again[c], ref[c]), "column %d, option off again" % c
+        with pytest.raises(gear.GearError):
+            t.set_options(8)
+        assert t.sync() == 0
+    finally:
+        t.close()
