@@ -827,8 +827,8 @@ def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=Fa
            "fallback": fallback}
     if pipelined and ng > 1:
         # Gather-stream time between one group's last gather and the next
-        # group's first: the handshake plus any wait for S.  About 12 us when
-        # the streams overlap; one group of selects and updates (about
+        # group's first: the handshake plus any wait for S.  About 9-13 us
+        # when the streams overlap; one group of selects and updates (about
         # 100 us) when they run one after the other.
         res["gather_stream_gap_us"] = float(np.median([hev.elapsed_ms(col_done[g - 1], col_begin[g]) * 1e3
                                                        for g in range(1, ng)]))
