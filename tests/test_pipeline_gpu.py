@@ -1,17 +1,22 @@
 """Selection and updates overlapping the gather on a second stream give the
-serial results bit for bit (the issue order of the benchmark's headline).
+serial results bit for bit, in the issue order of the benchmark's headline.
 
-Stream S runs the selects and updates of a group of steps, stream C the
-group's gathers after one event, and S reuses a buffer set only after C's
-event for it; the same table is also driven serially, on one stream, from
-the same insertions and seeds.  Indices, window starts, IS weights, every
-gathered byte and the final priorities must agree exactly, so the overlap
-changes timing only.  Run twice in each mode, this also checks that the
-same seeds give the same bytes (no race decides an output)."""
+Stream S runs the selects and updates of a group of steps and records one
+event after the group's last select; stream C waits for it and runs the
+group's gathers.  Groups follow the benchmark's schedule (one step, two,
+then `group`), the gathers of the first groups run with
+GEAR_OPT_GATHER_SHARE_CU as there, and S reuses a buffer set only after C's
+event for the group that last used it.  The same table is also driven
+serially, on one stream, from the same insertions and seeds.  Indices,
+window starts, IS weights, every gathered byte and the final priorities
+must agree exactly, so the overlap changes timing only.  Run twice in each
+mode, this also checks that the same seeds give the same bytes (no race
+decides an output)."""
 import numpy as np
 import pytest
 import torch
 
+import bench
 import gen
 from gen import configs
 from paper_2310_05205_amd import gear
@@ -52,32 +57,40 @@ def _run(pipelined, group=4):
                 record.append([host(idx[0]), host(start[0]), host(wts[0])] + [host(o) for o in outs[0]])
         else:
             C, S = torch.cuda.Stream(dev), torch.cuda.Stream(dev)
-            sel_done = [torch.cuda.Event() for _ in range(STEPS)]
-            col_done = [torch.cuda.Event() for _ in range(STEPS)]
-            ngroups = (STEPS + group - 1) // group
-            for g in range(ngroups):
-                js = range(g * group, min(STEPS, (g + 1) * group))
-                if g >= 2:
-                    S.wait_event(col_done[g - 2])
-                for j in js:
+            groups = bench.pipeline_groups(STEPS, group)
+            sel_done = [torch.cuda.Event() for _ in groups]
+            col_done = [torch.cuda.Event() for _ in groups]
+            pending = []  # gathered steps not yet read back, in step order
+
+            def read_back():
+                torch.cuda.synchronize(dev)
+                for j in pending:
+                    k = j % nsets
+                    record.append([host(idx[k]), host(start[k]), host(wts[k])] + [host(o) for o in outs[k]])
+                pending.clear()
+
+            for g, (js, waits) in enumerate(zip(groups, bench.set_reuse_waits(groups, nsets))):
+                if {j % nsets for j in js} & {j % nsets for j in pending}:
+                    read_back()  # before the group rewrites a set
+                for p in waits:
+                    S.wait_event(col_done[p])
+                for n, j in enumerate(js):
                     k = j % nsets
                     gear.gear_select(t.handle, gear.GEAR_PRIORITIZED, W.B, W.L, gen.select_seed(W.seed, j), W.beta,
                                      idx[k].data_ptr(), start[k].data_ptr(), wts[k].data_ptr(), S.cuda_stream)
+                    if n == len(js) - 1:
+                        sel_done[g].record(S)
                     gear.gear_update_priorities(t.handle, idx[k].data_ptr(), newp[j].data_ptr(), W.B, S.cuda_stream)
-                sel_done[g].record(S)
                 C.wait_event(sel_done[g])
+                t.set_options(gear.GEAR_OPT_GATHER_SHARE_CU if g < len(bench.RAMP) else 0)
                 for j in js:
                     k = j % nsets
                     gear.gear_collect(t.handle, idx[k].data_ptr(), start[k].data_ptr(), W.B, W.L, None,
                                       [o.data_ptr() for o in outs[k]], C.cuda_stream)
                 col_done[g].record(C)
-                if g % 2 == 1 or g == ngroups - 1:
-                    # Read back the finished groups before their sets are reused.
-                    torch.cuda.synchronize(dev)
-                    for gg in range(g - (g % 2), g + 1):
-                        for j in range(gg * group, min(STEPS, (gg + 1) * group)):
-                            k = j % nsets
-                            record.append([host(idx[k]), host(start[k]), host(wts[k])] + [host(o) for o in outs[k]])
+                pending.extend(js)
+            t.set_options(0)
+            read_back()
         torch.cuda.synchronize(dev)
         assert t.sync() == 0
         return record, t.priorities()
