@@ -96,6 +96,9 @@ def parse():
                     help="issue every step in order on one stream (default for batches under 128 MiB)")
     ap.add_argument("--pipeline", action="store_true",
                     help="overlap select/update with the gather on two streams whatever the batch size")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture the timed steps into one HIP graph and replay it (steps in order on one stream; "
+                         "only workloads whose calls replay correctly from a capture)")
     ap.add_argument("--group", type=int, default=4,
                     help="steps per cross-stream handshake when select/update overlap the gather")
     ap.add_argument("--legs", default="all", choices=["all", "headline"],
@@ -684,6 +687,19 @@ def concurrent_streams(dev, tries=8):
     return None  # e.g. under a counter-collecting profiler, which serialises dispatches
 
 
+def capturable(w, options):
+    """Whether a step of w (select, collect, and the update of prioritized or
+    TopK draws) replays correctly from a HIP graph capture: the calls whose
+    captures gear.h lists as replaying correctly."""
+    from paper_2310_05205_amd import gear
+    strategy = w.strategies[0]
+    if options & gear.GEAR_OPT_INCREMENTAL_TREE:
+        return strategy in (gear.GEAR_FIFO, gear.GEAR_LIFO, gear.GEAR_UNIFORM)
+    if strategy == gear.GEAR_PRIORITIZED:
+        return w.N <= gear.GEAR_SMALL_SELECT_MAX_N and w.B <= gear.GEAR_SMALL_SELECT_MAX_B
+    return True
+
+
 # Sizes of a pipeline's first groups.  The gather stream waits for the first
 # group's selections and updates before it can start, about 23 us per step
 # on an idle GPU, so the pipeline starts with one step, then two, then
@@ -723,7 +739,8 @@ def set_reuse_waits(groups, nsets):
     return waits
 
 
-def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=False, options=0):
+def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=False, options=0, timed_every=1,
+              graph=False):
     """W untimed steps, then K timed ones, of workload w on table t.
 
     Serial: select, collect and update of each step on one stream, in turn
@@ -745,12 +762,21 @@ def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=Fa
     Returns wall time, the mean gather launch time in the timed region, a
     per-stage breakdown from a one-stream loop after the timed region, and,
     with serial_too, the serial step time.  Gather launches are timed with
-    HIP events on C: serially, an event before and after each gather;
+    HIP events on C: serially, an event before and after the gather of every
+    timed_every-th step (each marker costs the stream about 2 us, which in a
+    launch-bound step of a few microseconds would dominate what is measured);
     pipelined, an event after C's wait and the group's closing event, which
-    bracket the group's gathers and nothing else."""
+    bracket the group's gathers and nothing else.
+
+    graph (serial steps only): the K timed steps are captured into one HIP
+    graph before the timed region, and the timed region replays it once.
+    Events cannot be recorded inside the graph, so the gather time then
+    comes from the stage loop after the timed region."""
     import numpy as np
     import torch
 
+    if graph and pipelined:
+        raise ValueError("graph replay takes steps issued in order on one stream")
     pair = concurrent_streams(dev) if pipelined else None
     fallback = pipelined and pair is None
     pipelined = pair is not None    # no two streams run concurrently: steps in order on one stream
@@ -760,6 +786,10 @@ def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=Fa
     if pipelined:
         gather_stream, side = pair
         C, S = ctypes.c_void_p(gather_stream.cuda_stream), ctypes.c_void_p(side.cuda_stream)
+    elif graph:
+        capture_stream = torch.cuda.Stream(dev)  # capture needs a stream other than the default one
+        C = ctypes.c_void_p(capture_stream.cuda_stream)
+        S = C
     else:
         C = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
         S = C
@@ -767,18 +797,19 @@ def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=Fa
     sel_done = [hev.create() for _ in range(ngroups)]
     col_begin = [hev.create() for _ in range(ngroups)]
     col_done = [hev.create() for _ in range(ngroups)]
-    ev = [(hev.create(), hev.create()) for _ in range(K)]
+    ev = [(hev.create(), hev.create()) for _ in range((K + timed_every - 1) // timed_every)]
 
     def loop_serial(its, timed):
         for j, it in enumerate(its):
             k = j % nsets
+            mark = timed and j % timed_every == 0
             step.select(it, k, C)
-            if timed:
-                hev.record(ev[j][0], C.value)
+            if mark:
+                hev.record(ev[j // timed_every][0], C.value)
             if step.ncols:
                 step.collect(k, C)
-            if timed:
-                hev.record(ev[j][1], C.value)
+            if mark:
+                hev.record(ev[j // timed_every][1], C.value)
             if step.updates:
                 step.update(it, k, C)
 
@@ -812,14 +843,25 @@ def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=Fa
     torch.cuda.synchronize()
     if t.sync() != 0:
         raise SystemExit("device status set during warm-up")
+    if graph:
+        hip_graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(hip_graph, stream=capture_stream, capture_error_mode="relaxed"):
+            loop_serial(range(W, W + K), False)
+        torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ng = loop_pipe(range(W, W + K)) if pipelined else loop_serial(range(W, W + K), True)
+    if graph:
+        hip_graph.replay()
+        ng = 0
+    else:
+        ng = loop_pipe(range(W, W + K)) if pipelined else loop_serial(range(W, W + K), True)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     status = t.sync()
     if status != 0:
         raise SystemExit("device status %d set during the timed steps" % status)
-    if pipelined:
+    if graph:
+        col_ms = None  # from the stage loop below
+    elif pipelined:
         col_ms = sum(hev.elapsed_ms(col_begin[g], col_done[g]) for g in range(ng)) / K
     else:
         col_ms = float(np.mean([hev.elapsed_ms(a, b) for a, b in ev]))
@@ -860,6 +902,8 @@ def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=Fa
               "collect": [hev.elapsed_ms(e[1], e[2]) for e in sev],
               "update": [hev.elapsed_ms(e[2], e[3]) for e in sev]}
     res["stages_mean"] = {k: float(np.mean(v)) for k, v in stages.items()}
+    if graph:
+        res["collect_ms"] = res["stages_mean"]["collect"]
     res["stages_pct"] = {k: [round(float(x), 5) for x in np.percentile(v, [10, 50, 90])] for k, v in stages.items()
                          if (k != "update" or step.updates) and (k != "collect" or step.ncols)}
     hev.close()
@@ -915,18 +959,25 @@ def host_link_leg(dev, steps=10, warmup=2):
             "cpu_staged": link["cpu_staged"], "table_setup_s": round(setup, 1)}
 
 
-def dt_full_leg(dev, launches=64, sets=8):
-    """DT-shaped table (6.55 GB, HBM), uniform selection of 512 whole
-    trajectories (L = T = 1000): 51.2 MB read and written per gather.  The
-    selections of `sets` batches are made first; then `launches` gathers run
-    back to back, cycling over those batches and their output buffers
-    (8 x 51.2 MB, more than the last-level cache holds), between two HIP
-    events on their stream."""
+def dt_legs(dev, launches=64, sets=8, window_steps=200):
+    """DT-shaped table (6.55 GB, HBM).
+
+    Whole trajectories: uniform selection of 512 whole trajectories (L = T =
+    1000), 51.2 MB read and written per gather.  The selections of `sets`
+    batches are made first; then `launches` gathers run back to back,
+    cycling over those batches and their output buffers (8 x 51.2 MB, more
+    than the last-level cache holds), between two HIP events on their stream.
+
+    20-step windows on the same table: `window_steps` steps of a uniform
+    select of 512 windows and their gather (2.05 MB), in order on one stream,
+    then the same steps captured into one HIP graph and replayed.  These
+    steps are launch-bound."""
     import torch
     from gen import configs
     w = configs.DT_FULL
     t = make_table(w)
     try:
+        windows = dt_windows(t, dev, window_steps)
         step = Step(t, w, sets, sets, dev)
         C = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
         for k in range(sets):
@@ -947,10 +998,29 @@ def dt_full_leg(dev, launches=64, sets=8):
     finally:
         t.close()
     roof = gather_roofline(w, col_ms, "dt-full")
-    return {"workload": w.name, "achieved_gbs": roof["achieved"], "peak_gbs": HBM_PEAK_GBS, "frac": roof["frac"],
+    full = {"workload": w.name, "achieved_gbs": roof["achieved"], "peak_gbs": HBM_PEAK_GBS, "frac": roof["frac"],
             "gate": 0.70, "avg_launch_ms": roof["avg_launch_ms"],
             "algorithmic_bytes_per_launch": roof["algorithmic_bytes_per_launch"], "traffic": roof["traffic"],
             "launches": launches, "batches": sets}
+    return full, windows
+
+
+def dt_windows(t, dev, K, W=10):
+    """The DT 20-step-window steps on table t (which holds the DT trajectories)."""
+    from gen import configs
+    w = configs.DT
+    eager = run_steps(t, w, K, W, dev, pipelined=False, stage_steps=20, timed_every=4)
+    replay = run_steps(t, w, K, W, dev, pipelined=False, stage_steps=20, graph=True)
+    ts = w.B * w.L * K
+    return {"workload": w.name, "strategy": "uniform", "steps": K,
+            "eager_us_per_step": round(eager["wall_s"] * 1e6 / K, 2),
+            "eager_value": round(ts / eager["wall_s"], 1),
+            "graph_us_per_step": round(replay["wall_s"] * 1e6 / K, 2),
+            "graph_value": round(ts / replay["wall_s"], 1),
+            "unit": "trajectory-steps/s",
+            "gather_avg_us": round(eager["collect_ms"] * 1e3, 2),
+            "note": "eager: select and gather issued in order on one stream, events around every 4th gather; "
+                    "graph: the same steps captured into one HIP graph before the timed region and replayed once"}
 
 
 def selection_leg(dev, iters=100, warmup=5):
@@ -1007,14 +1077,19 @@ def main():
 
     from paper_2310_05205_amd import gear
 
+    w = workload(args.workload)
+    opts = (gear.GEAR_OPT_INCREMENTAL_TREE if args.incremental else 0) | \
+        (gear.GEAR_OPT_IS_GLOBAL_MIN if args.global_min else 0)
+    if args.graph and not capturable(w, opts):
+        print("bench.py --graph: the %s steps cannot be replayed from a HIP graph capture (prioritized selection "
+              "over more than %d slots, or with the incremental tree, decides per call how to keep its sum tree)"
+              % (w.name, gear.GEAR_SMALL_SELECT_MAX_N), file=sys.stderr)
+        sys.exit(2)
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
     gear.lib()  # fails loudly if the library is not built
-    w = workload(args.workload)
     dev = torch.device("cuda", 0)
     t = make_table(w)
-    opts = (gear.GEAR_OPT_INCREMENTAL_TREE if args.incremental else 0) | \
-        (gear.GEAR_OPT_IS_GLOBAL_MIN if args.global_min else 0)
     if opts:
         t.set_options(opts)
     K, W = args.steps, args.warmup
@@ -1027,7 +1102,12 @@ def main():
     # and selection-only workloads, run in order on one stream.
     batch = w.B * w.L * sum(w.elem_bytes)
     pipelined = (batch >= PIPELINE_MIN_BATCH and not w.host_table and not args.serial) or args.pipeline
-    r = run_steps(t, w, K, W, dev, pipelined, group=args.group, serial_too=pipelined, options=opts)
+    if args.graph:
+        pipelined = False
+    # Short serial steps are launch-bound: time every fourth gather only.
+    timed_every = 1 if pipelined or batch >= PIPELINE_MIN_BATCH else 4
+    r = run_steps(t, w, K, W, dev, pipelined, group=args.group, serial_too=pipelined, options=opts,
+                  timed_every=timed_every, graph=args.graph)
     if r["fallback"]:
         print("bench.py: no two streams ran concurrently; the steps ran in order on one stream", file=sys.stderr)
     pipelined = r["pipelined"]
@@ -1063,9 +1143,12 @@ def main():
                    "tree": "incremental" if args.incremental and not args.global_min else "rescan per select",
                    "is_normalisation": "table minimum" if args.global_min else "batch minimum",
                    "steps_issued": "two streams, select/update overlapping the gather" if pipelined
-                   else "one stream, in order", "batch_buffer_sets": r["buffer_sets"],
+                   else "one HIP graph of the timed steps, captured before the timed region and replayed once"
+                   if args.graph else "one stream, in order", "batch_buffer_sets": r["buffer_sets"],
                    "steps_per_handshake": args.group if pipelined else None,
-                   "first_groups": [min(x, args.group) for x in RAMP] if pipelined else None},
+                   "first_groups": [min(x, args.group) for x in RAMP] if pipelined else None,
+                   "gathers_timed": "in the stage loop after the timed region (no events inside a graph)"
+                   if args.graph else "every step's" if timed_every == 1 else "every %dth step's" % timed_every},
         "roofline": roof,
         "cpu_baseline": cpu,
         "stages_ms": {"select": round(sm["select"], 5),
@@ -1087,7 +1170,7 @@ def main():
     if args.workload == "mat" and not (args.incremental or args.global_min) and args.legs == "all":
         # The other gates, measured in the same run after the headline table is closed.
         line["host_link"] = host_link_leg(dev)
-        line["dt_full"] = dt_full_leg(dev)
+        line["dt_full"], line["dt_windows"] = dt_legs(dev)
         line["selection"] = selection_leg(dev)
     print(json.dumps(line), flush=True)
 

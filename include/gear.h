@@ -42,13 +42,23 @@
  *     table, as long as the host calls still come from one thread and the
  *     index buffers it reads are not rewritten meanwhile.  Never concurrently
  *     with insertion, allocation or row writes, which change the columns.
- *   - HIP graph capture: gear_collect and gear_select_prioritized_noalloc
- *     keep no host-side state and may be captured and replayed.  Selection,
- *     insertion, allocation, commits and updates read and change host-side
- *     state when they are called (ring
- *     counters, whether the sum tree is current, which copy of its upper
- *     levels is live), so a replayed capture would repeat stale decisions:
- *     call them directly.
+ *   - HIP graph capture: a captured call replays the kernels and arguments
+ *     it chose when it was captured.  These calls choose them from nothing
+ *     that their replays change, so captures of them replay correctly:
+ *       gear_collect and gear_select_prioritized_noalloc;
+ *       gear_select with GEAR_FIFO, GEAR_LIFO, GEAR_UNIFORM or GEAR_TOPK,
+ *         and with GEAR_PRIORITIZED on a table of at most
+ *         GEAR_SMALL_SELECT_MAX_N slots, for batches of at most
+ *         GEAR_SMALL_SELECT_MAX_B and without GEAR_OPT_INCREMENTAL_TREE
+ *         (one launch, no sum tree);
+ *       gear_update_priorities without GEAR_OPT_INCREMENTAL_TREE.
+ *     They read the table's ring position, live count and options when
+ *     captured, so no insertion, allocation, commit or option change may
+ *     come between a capture and its replays.  Prioritized selection on
+ *     larger tables decides at each call whether to rebuild the sum tree,
+ *     and insertion, allocation and commits change host-side queues and
+ *     counters, so a replay would repeat stale decisions: call those
+ *     directly.
  *   - A HIP error left pending by an earlier call outside the library (a
  *     failed allocation, say) is cleared when a library call starts, so a
  *     return code describes only that call's own work.
@@ -110,6 +120,9 @@ extern "C" {
 #define GEAR_MAX_TOPK      16384        /* B limit of GEAR_TOPK */
 #define GEAR_NOALLOC_MAX_N (1 << 24)    /* N limit of gear_select_prioritized_noalloc */
 #define GEAR_NOALLOC_SCRATCH_BYTES 536832  /* its fixed device scratch per GPU */
+#define GEAR_SMALL_SELECT_MAX_N 16384  /* prioritized selection over at most this many slots, */
+#define GEAR_SMALL_SELECT_MAX_B 2048   /* for batches up to this size and without the incremental
+                                          tree, runs in one launch and keeps no sum tree */
 
 typedef struct gear_table gear_table;
 

@@ -23,8 +23,8 @@ constexpr int kMaxLevels = 6;
 // The search runs at most this many workgroups; each leaves the smallest
 // priority its draws selected in one slot of Table::wg_min.
 constexpr int kSearchMaxGrid = 2048;
-constexpr int64_t kSmallN = 16384;    // tables this small select in one launch (inclusive prefix in LDS)
-constexpr int32_t kSmallMaxB = 2048;  // ... for batches up to this size
+constexpr int64_t kSmallN = GEAR_SMALL_SELECT_MAX_N;  // tables this small select in one launch (prefix in LDS)
+constexpr int32_t kSmallMaxB = GEAR_SMALL_SELECT_MAX_B;  // ... for batches up to this size
 // TopK: at most this many workgroups per digit pass.
 constexpr int kTopkMaxGrid = 256;
 constexpr int kTopkBins = 4096;       // bins of one TopK digit pass (12-bit digits)

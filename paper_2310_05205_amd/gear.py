@@ -36,6 +36,8 @@ GEAR_MAX_BATCH = 1 << 24
 GEAR_MAX_TOPK = 16384
 GEAR_NOALLOC_MAX_N = 1 << 24
 GEAR_NOALLOC_SCRATCH_BYTES = 536832
+GEAR_SMALL_SELECT_MAX_N = 16384
+GEAR_SMALL_SELECT_MAX_B = 2048
 GEAR_OPT_INCREMENTAL_TREE = 1
 GEAR_OPT_IS_GLOBAL_MIN = 2
 GEAR_OPT_GATHER_SHARE_CU = 4

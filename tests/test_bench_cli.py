@@ -71,3 +71,20 @@ def test_buffer_sets_are_not_rewritten_before_their_gathers_end():
                 assert g - 1 not in ws
                 for j in js:
                     last[j % nsets] = g
+
+
+def test_graph_mode_only_for_steps_whose_captures_replay():
+    from gen import configs
+    from paper_2310_05205_amd import gear
+    assert bench.capturable(configs.DT, 0)
+    assert bench.capturable(configs.DT, gear.GEAR_OPT_INCREMENTAL_TREE)  # no update in a uniform step
+    assert bench.capturable(configs.TINY, 0)                             # one-launch prioritized selection
+    assert not bench.capturable(configs.TINY, gear.GEAR_OPT_INCREMENTAL_TREE)
+    assert bench.capturable(configs.TOPK_STRESS, 0)
+    assert not bench.capturable(configs.MAT, 0)                          # sum tree rebuilt per call
+    assert not bench.capturable(configs.GATO_HOST, 0)
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "mat", "--graph"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 2
+    assert "cannot be replayed" in r.stderr
+    assert r.stdout.strip() == ""
