@@ -110,7 +110,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target oracle time for the CPU baseline")
     ap.add_argument("--calibrate", action="store_true", help="run a plain copy kernel of known size and exit")
     ap.add_argument("--ceilings", action="store_true", help="measure plain read/write/copy HBM rates and exit")
-    return ap.parse_args()
+    args = ap.parse_args()
+    if args.group < 1:
+        ap.error("--group must be at least 1")
+    return args
 
 
 def workload(name):
@@ -717,6 +720,8 @@ RAMP = (1, 2)
 def pipeline_groups(n, group, ramp=RAMP):
     """Positions 0..n-1 split into handshake groups: the ramp's sizes (at most
     `group` each), then `group` steps per group."""
+    if group < 1:
+        raise ValueError("a handshake group holds at least one step")
     sizes = [min(r, group) for r in ramp]
     out, j, g = [], 0, 0
     while j < n:

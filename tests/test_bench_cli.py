@@ -88,3 +88,13 @@ def test_graph_mode_only_for_steps_whose_captures_replay():
     assert r.returncode == 2
     assert "cannot be replayed" in r.stderr
     assert r.stdout.strip() == ""
+
+
+def test_group_of_zero_steps_is_refused():
+    import pytest
+    with pytest.raises(ValueError):
+        bench.pipeline_groups(5, 0)
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--group", "0"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "--group" in r.stderr
