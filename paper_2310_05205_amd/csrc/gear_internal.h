@@ -29,7 +29,6 @@ constexpr int32_t kSmallMaxB = GEAR_SMALL_SELECT_MAX_B;  // ... for batches up t
 constexpr int kTopkMaxGrid = 256;
 constexpr int kTopkBins = 4096;       // bins of one TopK digit pass (12-bit digits)
 constexpr int kTopkStateWords = 32;   // TopK selection states after 0 .. 3 digit passes
-constexpr int kTopkRankBlock = 512;    // keys one TopK rank workgroup compares against
 constexpr int kTopkMaxK = GEAR_MAX_TOPK;
 // Host index and priority lists (row writes, allocation, commits) are
 // handled in chunks of kStageRows entries, through a ring of kStageSlots
@@ -104,7 +103,6 @@ struct Table {
     int pin_next = 0;                 // slot the next chunk uses
 
     uint64_t* topk_keys = nullptr;    // [kTopkMaxK] selected keys (p << 32 | ~slot), equal priorities in slot order
-    uint32_t* topk_rank = nullptr;    // [kTopkMaxK] place of each key in descending order
 };
 
 // Thread-local error reporting.

@@ -82,7 +82,6 @@ void free_table(Table* t) {
     (void)hipFree(t->topk_state);
     (void)hipFree(t->topk_local);
     (void)hipFree(t->topk_keys);
-    (void)hipFree(t->topk_rank);
     (void)hipFree(t->status);
     delete t;
 }
@@ -295,8 +294,7 @@ int create_table(const int64_t* elem_bytes, int32_t ncols, int64_t capacity, int
     if ((e = dmalloc(hook, &t->topk_hist, sizeof(uint32_t) * 3 * gear::kTopkBins)) != hipSuccess ||
         (e = dmalloc(hook, &t->topk_state, sizeof(uint32_t) * gear::kTopkStateWords)) != hipSuccess ||
         (e = dmalloc(hook, &t->topk_local, sizeof(uint32_t) * 3 * gear::kTopkMaxGrid * gear::kTopkBins)) != hipSuccess ||
-        (e = dmalloc(hook, &t->topk_keys, sizeof(uint64_t) * gear::kTopkMaxK)) != hipSuccess ||
-        (e = dmalloc(hook, &t->topk_rank, sizeof(uint32_t) * gear::kTopkMaxK)) != hipSuccess)
+        (e = dmalloc(hook, &t->topk_keys, sizeof(uint64_t) * gear::kTopkMaxK)) != hipSuccess)
         return oom("TopK scratch", e);
 
     if ((e = hipMemset(t->priority, 0, sizeof(uint32_t) * capacity)) != hipSuccess ||

@@ -30,12 +30,12 @@
 //                       loads orders its keys by slot.  It writes
 //                       (p << 32 | ~slot) of every slot above the threshold
 //                       and of the lowest-slot ones at it.
-//   topk_rank_kernel    a key's place in descending order is the number of
-//                       keys of higher priority plus those of equal priority
-//                       before it in the buffer (which is slot order); waves
-//                       count them over blocks of keys in parallel.
-//   topk_emit_kernel    writes slot, window start and weight at each key's
-//                       place, and clears the histograms for the next call.
+//   topk_rank_emit_kernel  a key's place in descending order is the number
+//                       of larger keys (keys hold the slot, so they are
+//                       unique); every workgroup stages all K keys in LDS
+//                       and ranks 32 of them, 32 lanes per key, then writes
+//                       slot, window start and weight at each key's place
+//                       and clears the histograms for the next call.
 //
 // Loads that a derivation waits for are issued before the bulk priority
 // loads: vector loads complete in issue order, so the reverse would make the
@@ -376,8 +376,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(const uint32
                                                                     const uint32_t* __restrict__ hist,
                                                                     const uint32_t* __restrict__ local, int grid,
                                                                     TopkState* __restrict__ states,
-                                                                    uint64_t* __restrict__ keys,
-                                                                    uint32_t* __restrict__ rank) {
+                                                                    uint64_t* __restrict__ keys) {
     __shared__ DeriveShared dsh;
     __shared__ uint32_t s_pre[kVec * kTopkWaves];  // per (load, wave): packed counts, then their prefix
     __shared__ uint64_t s_base[5];                 // above base, at base, total above, own above, own at
@@ -389,9 +388,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_compact_kernel(const uint32
     uint32_t v[kVec][4];
     load_batch(prio, lo, hi, v);
     const TopkState st = state_after(kPasses, stored, row, K, dsh);
-    if (blockIdx.x == 0 && threadIdx.x == 0) states[kPasses] = st;  // the final state, for rank and emit
-    // The rank kernel accumulates into rank: start it at zero.
-    for (int k = blockIdx.x * kTopkThreads + threadIdx.x; k < (int)K; k += grid * kTopkThreads) rank[k] = 0u;
+    if (blockIdx.x == 0 && threadIdx.x == 0) states[kPasses] = st;  // the final state, for the ranking
     uint64_t p_lo, p_hi;
     threshold_range(st, p_lo, p_hi);
     const uint64_t p_width = p_hi - p_lo;
@@ -494,82 +491,115 @@ __device__ __forceinline__ int selected(const TopkState& st, int32_t K) {
     return (st.flags & kAll) ? (int)st.total : K;
 }
 
-// Keys are unique (they hold the slot), so key i's place in descending
-// order is the number of larger keys.  blockIdx.x: 256 keys, one per thread;
-// blockIdx.y: a block of kRankBlock keys staged in LDS, read two at a time
-// with all lanes on the same address; the counts of all blocks are added
-// into rank[i].
-constexpr int kRankKeys = 256;
-constexpr int kRankBlock = kTopkRankBlock;
-static_assert(kRankBlock == 2 * kRankKeys, "each thread stages two keys of the block");
+// Rank and emit in one launch.  Keys are unique (they hold the slot), so a
+// key's place in descending order is the number of larger keys.  The
+// compaction wrote the n_gt keys above the threshold first, then those at
+// it, each group in slot order.  When every key at the threshold has the
+// same priority (the usual case: a threshold fixed to one value), a key at
+// it is preceded by all keys above and by the keys at it with lower slots,
+// so its place is its position in the list, and a key above the threshold
+// only needs comparing with the n_gt keys above it.  Otherwise every key is
+// compared with all n selected keys.
+//
+// Every workgroup stages the keys to compare with in LDS (positions past
+// them read as 0, below every key, since p >= 1) and ranks kEmitKeys keys,
+// kEmitLanes lanes per key each counting the larger keys among every
+// kEmitLanes-th pair of the staged list.  The lanes of one key read
+// consecutive pairs and the two keys of a wave read the same pairs, so every
+// LDS read is a conflict-free broadcast.  The counts are summed within each
+// 32-lane half of a wave, and the half's last lane writes slot, window start
+// and weight at its key's place.  Workgroups also clear the digit histograms
+// for the next call.
+constexpr int kEmitThreads = 1024;
+constexpr int kEmitLanes = 32;
+constexpr int kEmitKeys = kEmitThreads / kEmitLanes;
+constexpr int kEmitPad = 2 * kEmitLanes;  // staged keys per compare round (one pair per lane)
+static_assert(kTopkMaxK % kEmitPad == 0, "a padded key count never passes the key buffer");
+constexpr int kEmitLoads = kTopkMaxK / 2 / kEmitThreads;  // 16-byte loads per thread for the largest K
 
-__global__ __launch_bounds__(kRankKeys) void topk_rank_kernel(const uint64_t* __restrict__ keys,
-                                                              const TopkState* __restrict__ state, int32_t K,
-                                                              uint32_t* __restrict__ rank) {
-    __shared__ ulonglong2 blk[kRankBlock / 2];
-    const int i0 = blockIdx.x * kRankKeys;
-    const int j0 = blockIdx.y * kRankBlock;
-    const int i = i0 + (int)threadIdx.x;
-    // The state and every key this thread needs are loaded together (one
-    // memory round trip), from indices clamped into the K-entry buffer;
-    // entries at or past the selected count are then replaced.
-    const int ja = j0 + (int)threadIdx.x, jb = ja + kRankKeys;
-    const uint64_t ka = keys[ja < K ? ja : K - 1];
-    const uint64_t kb = keys[jb < K ? jb : K - 1];
-    const uint64_t km = keys[i < K ? i : K - 1];
-    const int n = selected(*state, K);
-    if (i0 >= n || j0 >= n) {
-        asm volatile("" ::"v"(ka), "v"(kb), "v"(km));  // no loads left in flight at the end
-        return;
-    }
-    uint64_t* b64 = reinterpret_cast<uint64_t*>(blk);
-    b64[threadIdx.x] = ja < n ? ka : 0ull;  // 0: below every key (p >= 1)
-    b64[threadIdx.x + kRankKeys] = jb < n ? kb : 0ull;
-    const uint64_t mine = i < n ? km : ~0ull;
-    __syncthreads();
-    uint32_t c0 = 0, c1 = 0;
-#pragma unroll 16
-    for (int q = 0; q < kRankBlock / 2; q++) {
-        const ulonglong2 y = blk[q];
-        c0 += y.x > mine;
-        c1 += y.y > mine;
-    }
-    if (i < n && c0 + c1) atomicAdd(&rank[i], c0 + c1);
+__device__ __forceinline__ ulonglong2 keep_below(ulonglong2 v, int e, int lim) {
+    return make_ulonglong2(2 * e < lim ? v.x : 0ull, 2 * e + 1 < lim ? v.y : 0ull);
 }
 
-__global__ void topk_emit_kernel(const uint64_t* __restrict__ keys, const uint32_t* __restrict__ rank,
-                                 const TopkState* __restrict__ state, int32_t K, uint64_t span, uint64_t seed,
-                                 int64_t* __restrict__ idx, int32_t* __restrict__ start, float* __restrict__ w,
-                                 uint32_t* status, uint32_t* __restrict__ hist) {
-    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    // The state, this thread's rank and its key are loaded together, from
-    // an index clamped into the K-entry buffers.
-    const int64_t tc = t < K ? t : K - 1;
-    const uint32_t b = rank[tc];  // for t < n: a permutation of 0 .. n-1
-    const uint64_t key = keys[tc];
+__global__ __launch_bounds__(kEmitThreads) void topk_rank_emit_kernel(const uint64_t* __restrict__ keys,
+                                                                      const TopkState* __restrict__ state, int32_t K,
+                                                                      uint64_t span, uint64_t seed,
+                                                                      int64_t* __restrict__ idx,
+                                                                      int32_t* __restrict__ start,
+                                                                      float* __restrict__ w, uint32_t* status,
+                                                                      uint32_t* __restrict__ hist) {
+    __shared__ ulonglong2 staged[kTopkMaxK / 2];
+    const int tid = (int)threadIdx.x;
+    const int pairs = (K + kEmitPad - 1) / kEmitPad * (kEmitPad / 2);  // within the kTopkMaxK-entry buffer
+    // The state, this thread's key and the first kEmitThreads pairs of the
+    // list are loaded together (one memory round trip), from indices
+    // clamped into the padded list.
+    const ulonglong2* kp = reinterpret_cast<const ulonglong2*>(keys);
+    const ulonglong2 v0 = kp[tid < pairs ? tid : pairs - 1];
+    const int i = blockIdx.x * kEmitKeys + tid / kEmitLanes;
+    const uint64_t km = keys[i < K ? i : K - 1];
     const TopkState st = *state;
     const int n = selected(st, K);
-    if (t < kPasses * kBins) hist[t] = 0u;  // every digit pass of this call is done
-    if (t == 0 && (st.flags & kInconsistent)) atomicOr(status, GEAR_STATUS_INTERNAL);
-    if (t >= K) {
-        asm volatile("" ::"v"(b), "v"(key));  // no loads left in flight at the end
-        return;
+    uint64_t p_lo, p_hi;
+    threshold_range(st, p_lo, p_hi);
+    const bool all = (st.flags & kAll) != 0;
+    int n_gt = all ? n : K - (int)st.k_rem;  // keys above the threshold, at the front of the list
+    n_gt = n_gt < 0 ? 0 : (n_gt < n ? n_gt : n);
+    const bool one = !all && p_hi - p_lo == 1;  // every key at the threshold has priority p_lo
+    const int lim = one ? n_gt : n;             // keys that some ranked key is compared with
+    const int pl = (lim + kEmitPad - 1) / kEmitPad * (kEmitPad / 2);  // staged pairs, <= pairs
+    if (tid < pl) staged[tid] = keep_below(v0, tid, lim);
+    if (pl > kEmitThreads) {  // the same branch for the whole workgroup
+        ulonglong2 v[kEmitLoads - 1];
+#pragma unroll
+        for (int k = 1; k < kEmitLoads; k++) {
+            const int e = k * kEmitThreads + tid;
+            v[k - 1] = kp[e < pl ? e : pl - 1];
+        }
+#pragma unroll
+        for (int k = 1; k < kEmitLoads; k++) {
+            const int e = k * kEmitThreads + tid;
+            if (e < pl) staged[e] = keep_below(v[k - 1], e, lim);
+        }
     }
-    if (t < n) {
-        if (b >= (uint32_t)n) {
+    for (int h = blockIdx.x * kEmitThreads + tid; h < kPasses * kBins; h += gridDim.x * kEmitThreads)
+        hist[h] = 0u;  // every digit pass of this call is done
+    if (blockIdx.x == 0 && tid == 0 && (st.flags & kInconsistent)) atomicOr(status, GEAR_STATUS_INTERNAL);
+    __syncthreads();
+    const int lane = tid & (kEmitLanes - 1);
+    const bool by_position = one && i >= n_gt;        // a key at a one-value threshold
+    const uint64_t mine = i < lim ? km : ~0ull;       // ~0: larger than every key, counts nothing
+    uint32_t c = 0;
+#pragma unroll 8
+    for (int q = lane; q < pl; q += kEmitLanes) {
+        const ulonglong2 y = staged[q];
+        c += (uint32_t)(y.x > mine) + (uint32_t)(y.y > mine);
+    }
+    // Sum over the 32 lanes of this key: row scans, then row 0's total into
+    // row 1 and row 2's into row 3, so lanes 31 and 63 hold the two keys' sums.
+    c += dpp32<0x111, 0xf>(c);
+    c += dpp32<0x112, 0xf>(c);
+    c += dpp32<0x114, 0xf>(c);
+    c += dpp32<0x118, 0xf>(c);
+    c += dpp32<0x142, 0xa>(c);
+    if (lane != kEmitLanes - 1 || i >= K) return;
+    if (i < n) {
+        const uint32_t b = by_position ? (uint32_t)i : c;
+        if (b >= (uint32_t)n) {  // a key list changed under a running selection
             atomicOr(status, GEAR_STATUS_INTERNAL);
             return;
         }
-        idx[b] = (int64_t)(0xFFFFFFFFu - (uint32_t)key);
+        idx[b] = (int64_t)(0xFFFFFFFFu - (uint32_t)km);
         start[b] = (int32_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b + 1), span);
         if (w) w[b] = 1.0f;
     } else {
-        idx[t] = -1;
-        start[t] = 0;
-        if (w) w[t] = 0.0f;
-        if (t == n) atomicOr(status, GEAR_STATUS_NO_WEIGHT);
+        idx[i] = -1;
+        start[i] = 0;
+        if (w) w[i] = 0.0f;
+        if (i == n) atomicOr(status, GEAR_STATUS_NO_WEIGHT);
     }
 }
+static_assert(kEmitLanes == 32 && kEmitThreads % 64 == 0, "the count sum covers the two halves of a wave");
 
 }  // namespace
 
@@ -592,15 +622,10 @@ hipError_t launch_topk(Table& t, int32_t K, int32_t L, uint64_t seed, int64_t* i
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     hipLaunchKernelGGL(topk_compact_kernel, dim3(grid), dim3(kTopkThreads), 0, s, t.priority, t.N, chunk,
-                       (uint32_t)K, t.topk_hist, t.topk_local, grid, states, t.topk_keys, t.topk_rank);
+                       (uint32_t)K, t.topk_hist, t.topk_local, grid, states, t.topk_keys);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(topk_rank_kernel, dim3((K + kRankKeys - 1) / kRankKeys, (K + kRankBlock - 1) / kRankBlock),
-                       dim3(kRankKeys), 0, s,
-                       t.topk_keys, state, K, t.topk_rank);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    const int emit = K > kPasses * kBins ? K : kPasses * kBins;
-    hipLaunchKernelGGL(topk_emit_kernel, dim3((emit + 255) / 256), dim3(256), 0, s, t.topk_keys, t.topk_rank, state,
-                       K, (uint64_t)(t.T - L + 1), seed, idx, start, w, t.status, t.topk_hist);
+    hipLaunchKernelGGL(topk_rank_emit_kernel, dim3((K + kEmitKeys - 1) / kEmitKeys), dim3(kEmitThreads), 0, s,
+                       t.topk_keys, state, K, (uint64_t)(t.T - L + 1), seed, idx, start, w, t.status, t.topk_hist);
     return hipGetLastError();
 }
 

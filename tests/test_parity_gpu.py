@@ -506,6 +506,39 @@ def test_topk_threshold_at_exponent_boundaries():
         t.close()
 
 
+def test_topk_threshold_bin_taken_whole():
+    """K ends exactly at the end of a digit bin that holds many distinct
+    priorities, so the threshold is a range of values, not one value: the
+    keys at it are in slot order but not in priority order and must be
+    ranked by comparison.  A bin of the first digit pass (from 2^20: 8192
+    values per bin), and one of the second (from 2^28 + 2^20: 512 values per
+    bin) whose first-pass bin also holds lower keys, so the first pass does
+    not decide."""
+    rng = np.random.default_rng(21)
+    N, T, M = 60000, 2, 3000
+    for base, width, lower in ((1 << 20, 8192, 0), ((1 << 28) + (1 << 20), 32, 1000)):
+        p = rng.integers(1, 1 << 12, N).astype(np.uint64)   # filler far below the bin
+        slots = rng.permutation(N)
+        inside, above, low = slots[:M], slots[M:M + 1500], slots[M + 1500:M + 1500 + lower]
+        p[inside] = base + rng.integers(0, width, M)
+        p[above] = rng.integers(base + (1 << 24), 1 << 32, above.size)
+        p[low] = (base & ~((1 << 21) - 1)) + rng.integers(0, 1000, lower)  # same first-pass bin, lower second-pass bin
+        p = p.astype(np.uint32)
+        t = gear.Table([1], capacity=N, T=T, residency=gear.GEAR_DEVICE, device=0)
+        try:
+            t.insert([np.zeros((N, T), np.uint8)], p)
+            for K in (above.size + M, above.size + M - 1, above.size + M + 1, above.size + 1, above.size):
+                say("TopK bin taken whole: base %#x, K=%d" % (base, K))
+                idx, start, wt = t.select(gear.GEAR_TOPK, K, 1, 9, 0.0, weights=True)
+                st, oidx, ostart, ow = oracle.select(oracle.TOPK, p, N, T, K, 1, 9, 0.0, True)
+                np.testing.assert_array_equal(host(idx), oidx, err_msg="base %#x K=%d" % (base, K))
+                np.testing.assert_array_equal(host(start), ostart)
+                np.testing.assert_array_equal(host(wt), ow)
+                assert t.sync() == (0 if st == oracle.OK else gear.GEAR_STATUS_NO_WEIGHT)
+        finally:
+            t.close()
+
+
 @pytest.mark.parametrize("global_min", [False, True], ids=["batch-min", "global-min"])
 def test_small_table_one_launch_and_tree_paths_alternate(global_min):
     """A table of at most 16384 slots selects in one launch for batches up
