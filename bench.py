@@ -915,6 +915,25 @@ def run_steps(t, w, K, W, dev, pipelined, group=4, stage_steps=50, serial_too=Fa
     return res
 
 
+def incremental_leg(t, w, dev, K=50, W=5):
+    """The same MAT table with the sum tree kept current by the updates
+    (GEAR_OPT_INCREMENTAL_TREE: selects skip the rescan), K steps in order
+    on one stream: the serial step and the select and update stage times.
+    The headline keeps the rescan per select that the method describes."""
+    from paper_2310_05205_amd import gear
+
+    t.set_options(gear.GEAR_OPT_INCREMENTAL_TREE)
+    r = run_steps(t, w, K, W, dev, False, stage_steps=K, options=gear.GEAR_OPT_INCREMENTAL_TREE)
+    t.set_options(0)
+    del r["step"]
+    sm, pct = r["stages_mean"], r["stages_pct"]
+    return {"tree": "incremental", "steps": K, "serial_ms_per_step": round(r["wall_s"] * 1e3 / K, 5),
+            "select_us": round(sm["select"] * 1e3, 2), "update_us": round(sm["update"] * 1e3, 2),
+            "collect_us": round(sm["collect"] * 1e3, 2),
+            "select_us_p10_p50_p90": [round(x * 1e3, 2) for x in pct["select"]],
+            "note": "steps in order on one stream on the headline table, the gathers timed by events"}
+
+
 def gather_roofline(w, col_ms, workload_key):
     """Roofline object of the gather: algorithmic bytes per launch over the
     mean event-timed launch duration."""
@@ -1127,6 +1146,9 @@ def main():
             raise SystemExit("the CPU-staged batch differs from the zero-copy batch")
         link["zero_copy_frac_of_h2d_copy"] = round(roof["achieved"] / link["link_h2d_copy_gbs"], 4)
     del r["step"]
+    incremental = None
+    if args.workload == "mat" and not (args.incremental or args.global_min) and args.legs == "all":
+        incremental = incremental_leg(t, w, dev)
     t.close()
 
     cpu = None
@@ -1177,6 +1199,7 @@ def main():
         line["host_link"] = host_link_leg(dev)
         line["dt_full"], line["dt_windows"] = dt_legs(dev)
         line["selection"] = selection_leg(dev)
+        line["incremental_tree"] = incremental
     print(json.dumps(line), flush=True)
 
 
