@@ -46,6 +46,7 @@
  *     it chose when it was captured.  These calls choose them from nothing
  *     that their replays change, so captures of them replay correctly:
  *       gear_collect and gear_select_prioritized_noalloc;
+ *       gear_select_collect;
  *       gear_select with GEAR_FIFO, GEAR_LIFO, GEAR_UNIFORM or GEAR_TOPK,
  *         and with GEAR_PRIORITIZED on a table of at most
  *         GEAR_SMALL_SELECT_MAX_N slots, for batches of at most
@@ -378,6 +379,29 @@ int gear_select(gear_table *t, int32_t strategy, int32_t B, int32_t L, uint64_t 
  */
 int gear_collect(gear_table *t, const int64_t *d_idx, const int32_t *d_start, int32_t B, int32_t L,
                  const int32_t *col_ids, int32_t ncols, void *const *d_out, void *stream);
+
+/*
+ * gear_select_collect - gear_select followed by gear_collect, in one launch,
+ * for the strategies whose draws are index arithmetic and counter-based
+ * random numbers (Sec. 3.3: FIFO and LIFO are deterministic, uniform
+ * sampling needs no weights), so the gather computes each window's slot and
+ * start itself instead of reading them from memory.  The results are those
+ * of gear_select(strategy, B, L, seed) with weights, then gear_collect over
+ * its d_idx and d_start: the same slots, starts, weights (all 1) and bytes.
+ *
+ *   strategy        GEAR_FIFO, GEAR_LIFO or GEAR_UNIFORM
+ *   B, L, seed      as for gear_select
+ *   d_idx, d_start  device int64[B], int32[B]: receive the draws
+ *   d_weights       device float[B] receiving 1 per draw, or NULL
+ *   col_ids, ncols, d_out  as for gear_collect
+ *
+ * Errors: GEAR_E_INVAL (NULL argument, another strategy, B, L or a column
+ * out of range; nothing enqueued), GEAR_E_EMPTY (nothing inserted),
+ * GEAR_E_INSUFFICIENT (FIFO/LIFO with B above the live count), GEAR_E_HIP.
+ */
+int gear_select_collect(gear_table *t, int32_t strategy, int32_t B, int32_t L, uint64_t seed, int64_t *d_idx,
+                        int32_t *d_start, float *d_weights, const int32_t *col_ids, int32_t ncols,
+                        void *const *d_out, void *stream);
 
 /*
  * Selection over G shards, one GPU's share (Sec. 3.3 centralized and

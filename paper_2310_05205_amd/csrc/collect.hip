@@ -77,13 +77,19 @@ struct ColTask {
     int32_t wpp;          // windows per piece (narrow)
     uint32_t epw;         // elements per window (narrow)
     uint32_t magic;       // ceil(2^32 / epw) for epw > 1: exact quotient for operands < 2^16
+    int32_t draws_out;    // 1: this column's pieces write the selected slots, starts and weights
 };
 
 struct CollectArgs {
     ColTask col[kMaxLaunchCols];
     int32_t ncols;
-    const int64_t* idx;
+    const int64_t* idx;     // the caller's draws, unless `computed`
     const int32_t* start;
+    int32_t computed;       // 1: FIFO, LIFO or uniform draws computed here from `draws`
+    SimpleDraws draws;
+    int64_t* idx_out;       // with `computed`: the draws, written by the pieces of a draws_out column
+    int32_t* start_out;
+    float* w_out;           // ... and weight 1 per draw, when not NULL
     int32_t B;
     int32_t T;
     int32_t L;
@@ -149,11 +155,21 @@ constexpr int64_t kNoWindow = -1;
 constexpr int64_t kBadWindow = -2;
 
 __device__ inline int64_t window_offset(const CollectArgs& a, const ColTask& c, int64_t b) {
+    if (a.computed) return (simple_slot(a.draws, b) * a.T + simple_start(a.draws, b)) * c.E;
     const int64_t i = a.idx[b];
     const int32_t s = a.start[b];
     if (i == -1) return kNoWindow;
     if (i < 0 || i >= a.N || s < 0 || s > a.T - a.L) return kBadWindow;
     return (i * a.T + s) * c.E;
+}
+
+// A gather that selects its own windows writes draw b's slot, start and
+// weight once: from the piece of the draws_out column that holds the
+// window's first element.
+__device__ inline void write_draw(const CollectArgs& a, int64_t b) {
+    a.idx_out[b] = simple_slot(a.draws, b);
+    a.start_out[b] = simple_start(a.draws, b);
+    if (a.w_out) a.w_out[b] = 1.0f;
 }
 
 // Piece q of a wide column: output elements [q*P, q*P + m) of the column's
@@ -173,6 +189,10 @@ __device__ void copy_wide(const CollectArgs& a, const ColTask& c, int64_t q) {
     const int64_t so0 = window_offset(a, c, w0);
     const int64_t so1 = two ? window_offset(a, c, w0 + 1) : kNoWindow;
     if (threadIdx.x == 0 && (so0 == kBadWindow || so1 == kBadWindow)) atomicOr(a.status, GEAR_STATUS_BAD_INDEX);
+    if (c.draws_out && threadIdx.x == 0) {  // a piece holds at most one window's first element
+        if (r0 == 0) write_draw(a, w0);
+        else if (two) write_draw(a, w0 + 1);
+    }
     const V* src = reinterpret_cast<const V*>(c.src);
     V* dst = reinterpret_cast<V*>(c.out) + o0;
     // Element offsets of the two windows' sources, shifted so that element
@@ -220,6 +240,7 @@ __device__ void copy_narrow(const CollectArgs& a, const ColTask& c, int64_t q) {
         const int64_t so = window_offset(a, c, b0 + threadIdx.x);
         s_off[threadIdx.x] = so < 0 ? -1 : so / WIDTH;
         if (so == kBadWindow) s_bad = 1;
+        if (c.draws_out) write_draw(a, b0 + threadIdx.x);
     }
     __syncthreads();
     if (threadIdx.x == 0 && s_bad) atomicOr(a.status, GEAR_STATUS_BAD_INDEX);
@@ -262,6 +283,104 @@ __global__ __launch_bounds__(kThreads) void collect_kernel(CollectArgs a) {
     }
 }
 
+// The collect launches over ncols requested columns (kMaxLaunchCols per
+// launch).  With `draws`, the windows are those FIFO, LIFO or uniform draws,
+// computed in the kernel, and the first launch's first column writes them to
+// idx_out, start_out and w_out; otherwise they come from idx and start.
+int launch_collect(Table* t, const int64_t* d_idx, const int32_t* d_start, const SimpleDraws* draws,
+                   int64_t* idx_out, int32_t* start_out, float* w_out, int32_t B, int32_t L,
+                   const int32_t* col_ids, int32_t ncols, void* const* d_out, hipStream_t s, const char* who) {
+    const bool pinned = t->residency == GEAR_HOST_PINNED;
+    int64_t batch_bytes = 0;
+    for (int j = 0; j < ncols; j++) batch_bytes += (int64_t)B * L * t->elem_bytes[col_ids ? col_ids[j] : j];
+    const int unroll = pinned ? kUnrollHost : batch_bytes >= kLargeBatch ? kUnrollLarge : kUnrollSmall;
+
+    for (int j0 = 0; j0 < ncols; j0 += kMaxLaunchCols) {
+        CollectArgs a{};
+        a.idx = d_idx;
+        a.start = d_start;
+        a.computed = draws != nullptr;
+        if (draws) {
+            a.draws = *draws;
+            a.idx_out = idx_out;
+            a.start_out = start_out;
+            a.w_out = w_out;
+        }
+        a.B = B;
+        a.T = t->T;
+        a.L = L;
+        a.N = t->N;
+        a.status = t->status;
+        a.ncols = 0;
+        int64_t tasks = 0;
+        // Tasks are numbered from the last requested column to the first:
+        // the wide columns, listed first in the common layouts, then end
+        // the launch with full pieces instead of small packed ones
+        // (measured 1.6% faster on whole 68 KB trajectories).
+        const int jend = ncols < j0 + kMaxLaunchCols ? ncols : j0 + kMaxLaunchCols;
+        for (int j = jend - 1; j >= j0; j--) {
+            const int c = col_ids ? col_ids[j] : j;
+            ColTask& ct = a.col[a.ncols++];
+            ct.src = t->col_dev[c];
+            ct.out = static_cast<uint8_t*>(d_out[j]);
+            ct.E = t->elem_bytes[c];
+            ct.W = (int64_t)L * ct.E;
+            ct.draws_out = draws != nullptr && j == 0;
+            const uintptr_t sa = reinterpret_cast<uintptr_t>(ct.src), oa = reinterpret_cast<uintptr_t>(ct.out);
+            // Window sources lie E bytes apart, or T*E when L = T (every
+            // window then starts at step 0); outputs lie W bytes apart.
+            const int64_t stride = L == t->T ? (int64_t)t->T * ct.E : ct.E;
+            if (stride % 16 == 0 && ct.W % 16 == 0 && sa % 16 == 0 && oa % 16 == 0) ct.width = 16;
+            else if (stride % 4 == 0 && ct.W % 4 == 0 && sa % 4 == 0 && oa % 4 == 0) ct.width = 4;
+            else ct.width = 1;
+            ct.piece = (int64_t)kThreads * unroll * ct.width;
+            ct.n = ct.W / ct.width;
+            ct.task0 = tasks;
+            if (ct.W >= ct.piece) {
+                ct.wide = 1;
+                ct.wpp = 1;
+                ct.epw = 0;
+                ct.magic = 0;
+                tasks += ((int64_t)B * ct.n + kThreads * unroll - 1) / (kThreads * unroll);
+            } else {
+                ct.wide = 0;
+                int64_t wpp = ct.piece / ct.W;
+                if (wpp > kThreads) wpp = kThreads;
+                ct.wpp = (int32_t)wpp;
+                ct.epw = (uint32_t)(ct.W / ct.width);
+                ct.magic = ct.epw > 1 ? (uint32_t)(((1ull << 32) + ct.epw - 1) / ct.epw) : 0u;
+                tasks += (B + wpp - 1) / wpp;
+            }
+        }
+        if (tasks > 0x7FFFFFFF) return fail(GEAR_E_INVAL, std::string(who) + ": batch too large for one launch");
+        const unsigned cap = (t->options & GEAR_OPT_GATHER_SHARE_CU) ? kShareLds : kCapLds;
+        const unsigned lds = !pinned && tasks >= kCapRounds * kResidentWorkgroups ? cap : 0u;
+        if (unroll == kUnrollLarge)
+            hipLaunchKernelGGL(collect_kernel<kUnrollLarge>, dim3((unsigned)tasks), dim3(kThreads), lds, s, a);
+        else if (unroll == kUnrollHost)
+            hipLaunchKernelGGL(collect_kernel<kUnrollHost>, dim3((unsigned)tasks), dim3(kThreads), lds, s, a);
+        else
+            hipLaunchKernelGGL(collect_kernel<kUnrollSmall>, dim3((unsigned)tasks), dim3(kThreads), lds, s, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, (std::string(who) + ": launch").c_str());
+    }
+    return GEAR_OK;
+}
+
+// Argument checks shared by gear_collect and gear_select_collect.
+int check_columns(const Table* t, const int32_t* col_ids, int32_t ncols, void* const* d_out, const char* who) {
+    if (d_out == nullptr) return fail(GEAR_E_INVAL, std::string(who) + ": NULL pointer argument");
+    if (col_ids == nullptr && ncols != t->ncols)
+        return fail(GEAR_E_INVAL, std::string(who) + ": ncols must equal the table's column count when col_ids is NULL");
+    if (ncols < 1 || ncols > GEAR_MAX_COLUMNS) return fail(GEAR_E_INVAL, std::string(who) + ": ncols out of range");
+    for (int j = 0; j < ncols; j++) {
+        const int c = col_ids ? col_ids[j] : j;
+        if (c < 0 || c >= t->ncols) return fail(GEAR_E_INVAL, std::string(who) + ": no such column");
+        if (d_out[j] == nullptr) return fail(GEAR_E_INVAL, std::string(who) + ": output pointer is NULL");
+    }
+    return GEAR_OK;
+}
+
 }  // namespace
 }  // namespace gear
 
@@ -274,88 +393,35 @@ extern "C" int gear_collect(gear_table* h, const int64_t* d_idx, const int32_t* 
     gear::Table* t = reinterpret_cast<gear::Table*>(h);
     if (B < 1 || B > GEAR_MAX_BATCH) return fail(GEAR_E_INVAL, "gear_collect: B out of range");
     if (L < 1 || L > t->T) return fail(GEAR_E_INVAL, "gear_collect: L must lie in [1, T]");
-    if (d_idx == nullptr || d_start == nullptr || d_out == nullptr)
-        return fail(GEAR_E_INVAL, "gear_collect: NULL pointer argument");
-    if (col_ids == nullptr && ncols != t->ncols)
-        return fail(GEAR_E_INVAL, "gear_collect: ncols must equal the table's column count when col_ids is NULL");
-    if (ncols < 1 || ncols > GEAR_MAX_COLUMNS) return fail(GEAR_E_INVAL, "gear_collect: ncols out of range");
-    for (int j = 0; j < ncols; j++) {
-        const int c = col_ids ? col_ids[j] : j;
-        if (c < 0 || c >= t->ncols) return fail(GEAR_E_INVAL, "gear_collect: no such column");
-        if (d_out[j] == nullptr) return fail(GEAR_E_INVAL, "gear_collect: output pointer is NULL");
-    }
+    if (d_idx == nullptr || d_start == nullptr) return fail(GEAR_E_INVAL, "gear_collect: NULL pointer argument");
+    int rc = gear::check_columns(t, col_ids, ncols, d_out, "gear_collect");
+    if (rc != GEAR_OK) return rc;
     gear::DeviceGuard guard(t->device);
     if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_collect: hipSetDevice");
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const bool pinned = t->residency == GEAR_HOST_PINNED;
-    int64_t batch_bytes = 0;
-    for (int j = 0; j < ncols; j++) batch_bytes += (int64_t)B * L * t->elem_bytes[col_ids ? col_ids[j] : j];
-    const int unroll = pinned ? gear::kUnrollHost
-                              : batch_bytes >= gear::kLargeBatch ? gear::kUnrollLarge : gear::kUnrollSmall;
+    return gear::launch_collect(t, d_idx, d_start, nullptr, nullptr, nullptr, nullptr, B, L, col_ids, ncols, d_out,
+                                static_cast<hipStream_t>(stream), "gear_collect");
+}
 
-    for (int j0 = 0; j0 < ncols; j0 += gear::kMaxLaunchCols) {
-        gear::CollectArgs a{};
-        a.idx = d_idx;
-        a.start = d_start;
-        a.B = B;
-        a.T = t->T;
-        a.L = L;
-        a.N = t->N;
-        a.status = t->status;
-        a.ncols = 0;
-        int64_t tasks = 0;
-        // Tasks are numbered from the last requested column to the first:
-        // the wide columns, listed first in the common layouts, then end
-        // the launch with full pieces instead of small packed ones
-        // (measured 1.6% faster on whole 68 KB trajectories).
-        const int jend = ncols < j0 + gear::kMaxLaunchCols ? ncols : j0 + gear::kMaxLaunchCols;
-        for (int j = jend - 1; j >= j0; j--) {
-            const int c = col_ids ? col_ids[j] : j;
-            gear::ColTask& ct = a.col[a.ncols++];
-            ct.src = t->col_dev[c];
-            ct.out = static_cast<uint8_t*>(d_out[j]);
-            ct.E = t->elem_bytes[c];
-            ct.W = (int64_t)L * ct.E;
-            const uintptr_t sa = reinterpret_cast<uintptr_t>(ct.src), oa = reinterpret_cast<uintptr_t>(ct.out);
-            // Window sources lie E bytes apart, or T*E when L = T (every
-            // window then starts at step 0); outputs lie W bytes apart.
-            const int64_t stride = L == t->T ? (int64_t)t->T * ct.E : ct.E;
-            if (stride % 16 == 0 && ct.W % 16 == 0 && sa % 16 == 0 && oa % 16 == 0) ct.width = 16;
-            else if (stride % 4 == 0 && ct.W % 4 == 0 && sa % 4 == 0 && oa % 4 == 0) ct.width = 4;
-            else ct.width = 1;
-            ct.piece = (int64_t)gear::kThreads * unroll * ct.width;
-            ct.n = ct.W / ct.width;
-            ct.task0 = tasks;
-            if (ct.W >= ct.piece) {
-                ct.wide = 1;
-                ct.wpp = 1;
-                ct.epw = 0;
-                ct.magic = 0;
-                tasks += ((int64_t)B * ct.n + gear::kThreads * unroll - 1) / (gear::kThreads * unroll);
-            } else {
-                ct.wide = 0;
-                int64_t wpp = ct.piece / ct.W;
-                if (wpp > gear::kThreads) wpp = gear::kThreads;
-                ct.wpp = (int32_t)wpp;
-                ct.epw = (uint32_t)(ct.W / ct.width);
-                ct.magic = ct.epw > 1 ? (uint32_t)(((1ull << 32) + ct.epw - 1) / ct.epw) : 0u;
-                tasks += (B + wpp - 1) / wpp;
-            }
-        }
-        if (tasks > 0x7FFFFFFF) return fail(GEAR_E_INVAL, "gear_collect: batch too large for one launch");
-        const unsigned cap = (t->options & GEAR_OPT_GATHER_SHARE_CU) ? gear::kShareLds : gear::kCapLds;
-        const unsigned lds = !pinned && tasks >= gear::kCapRounds * gear::kResidentWorkgroups ? cap : 0u;
-        if (unroll == gear::kUnrollLarge)
-            hipLaunchKernelGGL(gear::collect_kernel<gear::kUnrollLarge>, dim3((unsigned)tasks), dim3(gear::kThreads),
-                               lds, s, a);
-        else if (unroll == gear::kUnrollHost)
-            hipLaunchKernelGGL(gear::collect_kernel<gear::kUnrollHost>, dim3((unsigned)tasks), dim3(gear::kThreads),
-                               lds, s, a);
-        else
-            hipLaunchKernelGGL(gear::collect_kernel<gear::kUnrollSmall>, dim3((unsigned)tasks), dim3(gear::kThreads),
-                               lds, s, a);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return hip_fail(e, "gear_collect: launch");
-    }
-    return GEAR_OK;
+extern "C" int gear_select_collect(gear_table* h, int32_t strategy, int32_t B, int32_t L, uint64_t seed,
+                                   int64_t* d_idx, int32_t* d_start, float* d_weights, const int32_t* col_ids,
+                                   int32_t ncols, void* const* d_out, void* stream) {
+    if (h == nullptr) return fail(GEAR_E_INVAL, "gear_select_collect: table is NULL");
+    gear::Table* t = reinterpret_cast<gear::Table*>(h);
+    if (strategy != GEAR_FIFO && strategy != GEAR_LIFO && strategy != GEAR_UNIFORM)
+        return fail(GEAR_E_INVAL, "gear_select_collect: strategy must be GEAR_FIFO, GEAR_LIFO or GEAR_UNIFORM");
+    if (B < 1 || B > GEAR_MAX_BATCH) return fail(GEAR_E_INVAL, "gear_select_collect: B out of range");
+    if (L < 1 || L > t->T) return fail(GEAR_E_INVAL, "gear_select_collect: L must lie in [1, T]");
+    if (d_idx == nullptr || d_start == nullptr)
+        return fail(GEAR_E_INVAL, "gear_select_collect: NULL pointer argument");
+    int rc = gear::check_columns(t, col_ids, ncols, d_out, "gear_select_collect");
+    if (rc != GEAR_OK) return rc;
+    const int64_t live = gear::live_count(*t);
+    if (live == 0) return fail(GEAR_E_EMPTY, "gear_select_collect: nothing inserted");
+    if ((strategy == GEAR_FIFO || strategy == GEAR_LIFO) && (int64_t)B > live)
+        return fail(GEAR_E_INSUFFICIENT, "gear_select_collect: FIFO/LIFO batch larger than the live count");
+    gear::DeviceGuard guard(t->device);
+    if (guard.error() != hipSuccess) return hip_fail(guard.error(), "gear_select_collect: hipSetDevice");
+    const gear::SimpleDraws d = gear::simple_draws(*t, strategy, L, seed);
+    return gear::launch_collect(t, nullptr, nullptr, &d, d_idx, d_start, d_weights, B, L, col_ids, ncols, d_out,
+                                static_cast<hipStream_t>(stream), "gear_select_collect");
 }

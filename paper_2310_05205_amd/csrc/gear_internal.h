@@ -8,6 +8,7 @@
 #include <vector>
 
 #include "gear.h"
+#include "wave.h"
 
 namespace gear {
 
@@ -151,6 +152,9 @@ hipError_t launch_topk(Table& t, int32_t K, int32_t L, uint64_t seed, int64_t* i
                        hipStream_t s);
 hipError_t launch_simple_select(Table& t, int32_t strategy, int32_t B, int32_t L, uint64_t seed,
                                 int64_t* idx, int32_t* start, float* w, hipStream_t s);
+// The arguments of FIFO, LIFO or uniform draws from the table's current ring
+// (or commit-order) state; the table must have a live entry.
+SimpleDraws simple_draws(const Table& t, int32_t strategy, int32_t L, uint64_t seed);
 // With maintain_tree, the scatter also adds new - old of every changed
 // slot into the sum tree the last scan filled.
 hipError_t launch_scatter(Table& t, const int64_t* idx, const uint32_t* newp, int32_t B, bool maintain_tree,

@@ -420,29 +420,12 @@ __global__ __launch_bounds__(kSmallThreads) void small_select_kernel(const uint3
 // A ring table's positions are its slots, and its live slots are [0, n).
 // A managed table (index manager) reads the slot at each position of its
 // commit-order ring `order`, oldest commit at `oldest`.
-__global__ void simple_select_kernel(int strategy, int32_t B, int64_t N, int64_t live, int64_t oldest,
-                                     int64_t newest, const int32_t* __restrict__ order, uint64_t span,
-                                     uint64_t seed, int64_t* __restrict__ idx, int32_t* __restrict__ start,
-                                     float* __restrict__ w) {
+__global__ void simple_select_kernel(SimpleDraws d, int32_t B, int64_t* __restrict__ idx,
+                                     int32_t* __restrict__ start, float* __restrict__ w) {
     const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= B) return;
-    int64_t i;
-    if (strategy == GEAR_FIFO) {
-        i = oldest + b;
-        if (i >= N) i -= N;
-    } else if (strategy == GEAR_LIFO) {
-        i = newest - b;
-        if (i < 0) i += N;
-    } else {
-        i = (int64_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b), (uint64_t)live);
-        if (order) {
-            i += oldest;
-            if (i >= N) i -= N;
-        }
-    }
-    if (order) i = order[i];
-    idx[b] = i;
-    start[b] = (int32_t)scale_draw(splitmix64_out(seed, 2 * (uint64_t)b + 1), span);
+    idx[b] = simple_slot(d, b);
+    start[b] = simple_start(d, b);
     if (w) w[b] = 1.0f;
 }
 
@@ -528,20 +511,28 @@ hipError_t launch_small_select(Table& t, int32_t B, int32_t L, uint64_t seed, fl
     return hipGetLastError();
 }
 
+SimpleDraws simple_draws(const Table& t, int32_t strategy, int32_t L, uint64_t seed) {
+    SimpleDraws d{};
+    d.strategy = strategy;
+    d.N = t.N;
+    d.live = live_count(t);
+    if (t.managed) {
+        d.oldest = t.ord_head;
+        d.newest = (t.ord_head + d.live - 1) % t.N;
+    } else {
+        d.oldest = (int64_t)((t.next_seq - (uint64_t)d.live) % (uint64_t)t.N);
+        d.newest = (int64_t)((t.next_seq - 1) % (uint64_t)t.N);
+    }
+    d.order = t.managed ? t.order : nullptr;
+    d.span = (uint64_t)(t.T - L + 1);
+    d.seed = seed;
+    return d;
+}
+
 hipError_t launch_simple_select(Table& t, int32_t strategy, int32_t B, int32_t L, uint64_t seed, int64_t* idx,
                                 int32_t* start, float* w, hipStream_t s) {
-    const int64_t live = live_count(t);
-    int64_t oldest, newest;
-    if (t.managed) {
-        oldest = t.ord_head;
-        newest = (t.ord_head + live - 1) % t.N;
-    } else {
-        oldest = (int64_t)((t.next_seq - (uint64_t)live) % (uint64_t)t.N);
-        newest = (int64_t)((t.next_seq - 1) % (uint64_t)t.N);
-    }
-    hipLaunchKernelGGL(simple_select_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s, strategy, B, t.N,
-                       live, oldest, newest, t.managed ? t.order : nullptr, (uint64_t)(t.T - L + 1), seed, idx,
-                       start, w);
+    hipLaunchKernelGGL(simple_select_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s,
+                       simple_draws(t, strategy, L, seed), B, idx, start, w);
     return hipGetLastError();
 }
 

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "gear.h"
+
 namespace gear {
 
 // splitmix64 (Steele, Lea & Flood, OOPSLA 2014): output c of the stream
@@ -18,6 +20,44 @@ __device__ __forceinline__ uint64_t splitmix64_out(uint64_t seed, uint64_t c) {
 
 // floor(u * n / 2^64): the high word of the 128-bit product.
 __device__ __forceinline__ uint64_t scale_draw(uint64_t u, uint64_t n) { return __umul64hi(u, n); }
+
+// Draw b of a FIFO, LIFO or uniform selection (Sec. 3.3): a slot from
+// index arithmetic on the ring of live slots (or on the commit order of a
+// table with an index manager, when `order` is not NULL), and a window start
+// drawn from splitmix64 output 2b + 1.  gear_select's kernel and the gather
+// that selects its own windows both call these, so the two agree bit for bit.
+struct SimpleDraws {
+    int32_t strategy;       // GEAR_FIFO, GEAR_LIFO or GEAR_UNIFORM
+    int64_t N;              // capacity
+    int64_t live;           // live count (>= 1)
+    int64_t oldest;         // ring (or commit-order) position of the oldest live entry
+    int64_t newest;         // ... and of the newest
+    const int32_t* order;   // commit order [N] of a managed table, else NULL
+    uint64_t span;          // T - L + 1 window starts
+    uint64_t seed;
+};
+
+__device__ __forceinline__ int64_t simple_slot(const SimpleDraws& d, int64_t b) {
+    int64_t i;
+    if (d.strategy == GEAR_FIFO) {
+        i = d.oldest + b;
+        if (i >= d.N) i -= d.N;
+    } else if (d.strategy == GEAR_LIFO) {
+        i = d.newest - b;
+        if (i < 0) i += d.N;
+    } else {
+        i = (int64_t)scale_draw(splitmix64_out(d.seed, 2 * (uint64_t)b), (uint64_t)d.live);
+        if (d.order) {
+            i += d.oldest;
+            if (i >= d.N) i -= d.N;
+        }
+    }
+    return d.order ? (int64_t)d.order[i] : i;
+}
+
+__device__ __forceinline__ int32_t simple_start(const SimpleDraws& d, int64_t b) {
+    return (int32_t)scale_draw(splitmix64_out(d.seed, 2 * (uint64_t)b + 1), d.span);
+}
 
 // Wave-level scans with DPP (gfx9 data-parallel primitives, all 64 lanes
 // active): row shifts by 1, 2, 4, 8 scan each row of 16 lanes, then the

@@ -82,6 +82,7 @@ def lib():
         L.gear_insert.argtypes = [vp, i64, vp, vp, vp]
         L.gear_select.argtypes = [vp, i32, i32, i32, u64, ctypes.c_float, vp, vp, vp, vp]
         L.gear_collect.argtypes = [vp, vp, vp, i32, i32, vp, i32, vp, vp]
+        L.gear_select_collect.argtypes = [vp, i32, i32, i32, u64, vp, vp, vp, vp, i32, vp, vp]
         L.gear_update_priorities.argtypes = [vp, vp, vp, i32, vp]
         L.gear_table_sync.argtypes = [vp, vp, ctypes.POINTER(i32)]
         L.gear_table_info.argtypes = [vp, ctypes.POINTER(i64), ctypes.POINTER(u64)]
@@ -105,6 +106,7 @@ def lib():
                                              ctypes.POINTER(i32)]
         L.gear_table_find_column.argtypes = [vp, ctypes.c_char_p, ctypes.POINTER(i32)]
         for name in ["gear_table_create", "gear_table_destroy", "gear_insert", "gear_select", "gear_collect",
+                     "gear_select_collect",
                      "gear_update_priorities", "gear_table_sync", "gear_table_info", "gear_table_column",
                      "gear_table_priorities", "gear_table_set_options", "gear_table_use_allocator",
                      "gear_allocate", "gear_commit", "gear_allocator_info", "gear_write_rows", "gear_shard_total",
@@ -195,6 +197,14 @@ def gear_collect(table, d_idx, d_start, B, L, col_ids, d_out, stream=0):
     """col_ids: list of column numbers or None (all); d_out: list of device pointers."""
     ids = (ctypes.c_int32 * len(col_ids))(*col_ids) if col_ids is not None else None
     _check(lib().gear_collect(table, d_idx, d_start, int(B), int(L), ids, len(d_out), _ptr_array(d_out), stream))
+
+
+def gear_select_collect(table, strategy, B, L, seed, d_idx, d_start, d_weights, col_ids, d_out, stream=0):
+    """FIFO, LIFO or uniform selection and the gather of its windows in one
+    launch; col_ids: list of column numbers or None (all)."""
+    ids = (ctypes.c_int32 * len(col_ids))(*col_ids) if col_ids is not None else None
+    _check(lib().gear_select_collect(table, int(strategy), int(B), int(L), int(seed) & ((1 << 64) - 1), d_idx,
+                                     d_start, d_weights or None, ids, len(d_out), _ptr_array(d_out), stream))
 
 
 def gear_update_priorities(table, d_idx, d_new_priorities, B, stream=0):
@@ -433,6 +443,22 @@ class Table:
         gear_collect(self.handle, idx.data_ptr(), start.data_ptr(), B, L, col_ids,
                      [o.data_ptr() for o in out], self._stream(stream))
         return out
+
+    def select_collect(self, strategy, B, L, seed, weights=False, col_ids=None, stream=None):
+        """FIFO, LIFO or uniform selection and its gather in one launch:
+        (idx, start, w, list of uint8 tensors [B, L*E_c]), equal to select()
+        followed by collect()."""
+        torch = self._torch
+        dev = torch.device("cuda", self.device)
+        idx = torch.empty(B, dtype=torch.int64, device=dev)
+        start = torch.empty(B, dtype=torch.int32, device=dev)
+        w = torch.empty(B, dtype=torch.float32, device=dev) if weights else None
+        cols = list(range(len(self.elem_bytes))) if col_ids is None else list(col_ids)
+        out = [torch.empty((B, L * self.elem_bytes[c]), dtype=torch.uint8, device=dev) for c in cols]
+        gear_select_collect(self.handle, strategy, B, L, seed, idx.data_ptr(), start.data_ptr(),
+                            w.data_ptr() if w is not None else 0, col_ids, [o.data_ptr() for o in out],
+                            self._stream(stream))
+        return idx, start, w, out
 
     def collect_fields(self, idx, start, L, fields=None, stream=None, out=None):
         """The batch as {name: tensor[B, L, *shape]} of each column's dtype
