@@ -99,6 +99,9 @@ def parse():
     ap.add_argument("--graph", action="store_true",
                     help="capture the timed steps into one HIP graph and replay it (steps in order on one stream; "
                          "only workloads whose calls replay correctly from a capture)")
+    ap.add_argument("--fused", action="store_true",
+                    help="FIFO, LIFO and uniform workloads: each step is one gear_select_collect launch "
+                         "(selection computed inside the gather)")
     ap.add_argument("--group", type=int, default=4,
                     help="steps per cross-stream handshake when select/update overlap the gather")
     ap.add_argument("--legs", default="all", choices=["all", "headline"],
@@ -644,6 +647,12 @@ class Step:
         self._ok(self.lib.gear_update_priorities(self.tab, self.ip[k], self.np_[it], self.B, sh),
                  "gear_update_priorities")
 
+    def select_collect(self, it, k, sh):
+        """FIFO, LIFO or uniform selection and its gather in one launch."""
+        self._ok(self.lib.gear_select_collect(self.tab, self.strategy, self.B, self.L, self.seeds[it], self.ip[k],
+                                              self.sp[k], self.wp[k], None, self.ncols, self.op[k], sh),
+                 "gear_select_collect")
+
     def share_cus(self, on):
         """Gathers enqueued from now on leave room for the other stream (on) or not."""
         opts = self.options | (self.gear.GEAR_OPT_GATHER_SHARE_CU if on else 0)
@@ -983,6 +992,58 @@ def host_link_leg(dev, steps=10, warmup=2):
             "cpu_staged": link["cpu_staged"], "table_setup_s": round(setup, 1)}
 
 
+def run_fused(t, w, K, W, dev, graph=False, timed_every=4):
+    """K steps of gear_select_collect (FIFO, LIFO or uniform selection and
+    its gather in one launch) in order on one stream, after W untimed ones,
+    over two buffer sets.  Eager: HIP events around every timed_every-th
+    launch.  graph: the K steps captured into one HIP graph before the timed
+    region, which replays it once.  Returns wall seconds and the mean event-
+    timed launch (None with graph)."""
+    import numpy as np
+    import torch
+
+    step = Step(t, w, 2, W + K, dev)
+    hev = HipEvents()
+    ev = [(hev.create(), hev.create()) for _ in range((K + timed_every - 1) // timed_every)]
+    if graph:
+        cs = torch.cuda.Stream(dev)
+        C = ctypes.c_void_p(cs.cuda_stream)
+    else:
+        C = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+
+    def loop(its, timed):
+        for j, it in enumerate(its):
+            mark = timed and j % timed_every == 0
+            if mark:
+                hev.record(ev[j // timed_every][0], C.value)
+            step.select_collect(it, j % 2, C)
+            if mark:
+                hev.record(ev[j // timed_every][1], C.value)
+
+    if graph:
+        with torch.cuda.stream(cs):
+            loop(range(W), False)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cs, capture_error_mode="relaxed"):
+            loop(range(W, W + K), False)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        g.replay()
+    else:
+        loop(range(W), False)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        loop(range(W, W + K), True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = None if graph else float(np.mean([hev.elapsed_ms(a, b) for a, b in ev]))
+    hev.close()
+    if t.sync() != 0:
+        raise SystemExit("device status set during the fused select-and-gather steps")
+    return wall, ms
+
+
 def dt_legs(dev, launches=64, sets=8, window_steps=200):
     """DT-shaped table (6.55 GB, HBM).
 
@@ -1016,6 +1077,15 @@ def dt_legs(dev, launches=64, sets=8, window_steps=200):
         hev.record(b, C.value)
         torch.cuda.synchronize()
         col_ms = hev.elapsed_ms(a, b) / launches
+        # The same batches selected inside the gather launch (uniform draws
+        # computed per piece, no index list read first), back to back.
+        a2, b2 = hev.create(), hev.create()
+        hev.record(a2, C.value)
+        for k in range(launches):
+            step.select_collect(k % sets, k % sets, C)
+        hev.record(b2, C.value)
+        torch.cuda.synchronize()
+        fused_ms = hev.elapsed_ms(a2, b2) / launches
         hev.close()
         if t.sync() != 0:
             raise SystemExit("device status set during the whole-trajectory gathers")
@@ -1026,6 +1096,11 @@ def dt_legs(dev, launches=64, sets=8, window_steps=200):
             "gate": 0.70, "avg_launch_ms": roof["avg_launch_ms"],
             "algorithmic_bytes_per_launch": roof["algorithmic_bytes_per_launch"], "traffic": roof["traffic"],
             "launches": launches, "batches": sets}
+    fused = gather_roofline(w, fused_ms, "dt-full")
+    full["select_collect"] = {"avg_launch_ms": fused["avg_launch_ms"], "achieved_gbs": fused["achieved"],
+                              "frac": fused["frac"],
+                              "note": "gear_select_collect: the uniform selection computed inside the gather launch, "
+                                      "the same bytes per launch"}
     return full, windows
 
 
@@ -1035,6 +1110,8 @@ def dt_windows(t, dev, K, W=10):
     w = configs.DT
     eager = run_steps(t, w, K, W, dev, pipelined=False, stage_steps=20, timed_every=4)
     replay = run_steps(t, w, K, W, dev, pipelined=False, stage_steps=20, graph=True)
+    f_wall, f_ms = run_fused(t, w, K, W, dev)
+    g_wall, _ = run_fused(t, w, K, W, dev, graph=True)
     ts = w.B * w.L * K
     return {"workload": w.name, "strategy": "uniform", "steps": K,
             "eager_us_per_step": round(eager["wall_s"] * 1e6 / K, 2),
@@ -1043,8 +1120,12 @@ def dt_windows(t, dev, K, W=10):
             "graph_value": round(ts / replay["wall_s"], 1),
             "unit": "trajectory-steps/s",
             "gather_avg_us": round(eager["collect_ms"] * 1e3, 2),
+            "select_collect": {"eager_us_per_step": round(f_wall * 1e6 / K, 2), "eager_value": round(ts / f_wall, 1),
+                               "graph_us_per_step": round(g_wall * 1e6 / K, 2), "graph_value": round(ts / g_wall, 1),
+                               "launch_avg_us": round(f_ms * 1e3, 2)},
             "note": "eager: select and gather issued in order on one stream, events around every 4th gather; "
-                    "graph: the same steps captured into one HIP graph before the timed region and replayed once"}
+                    "graph: the same steps captured into one HIP graph before the timed region and replayed once; "
+                    "select_collect: each step one gear_select_collect launch, eager and from a graph"}
 
 
 def selection_leg(dev, iters=100, warmup=5):
@@ -1125,6 +1206,24 @@ def main():
     # step); a pinned host table's gather takes milliseconds; so those steps,
     # and selection-only workloads, run in order on one stream.
     batch = w.B * w.L * sum(w.elem_bytes)
+    if args.fused:
+        if strategy not in (gear.GEAR_FIFO, gear.GEAR_LIFO, gear.GEAR_UNIFORM) or not w.elem_bytes:
+            print("bench.py --fused: only FIFO, LIFO and uniform workloads with columns", file=sys.stderr)
+            sys.exit(2)
+        wall, ms = run_fused(t, w, K, W, dev, graph=args.graph, timed_every=1 if batch >= PIPELINE_MIN_BATCH else 4)
+        t.close()
+        line = {"metric": METRIC, "value": round(w.B * w.L * K / wall, 1), "unit": "trajectory-steps/s",
+                "n_gpus": 1, "steps": K, "warmup": W, "ms_per_step": round(wall * 1e3 / K, 5),
+                "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u64",
+                "data": "synthetic",
+                "config": {"workload": w.name, "N": w.N, "T": w.T, "B": w.B, "L": w.L,
+                           "strategy": {0: "fifo", 1: "lifo", 2: "uniform"}[strategy],
+                           "steps_issued": "one gear_select_collect launch per step, "
+                                           + ("replayed from a HIP graph" if args.graph else "in order on one stream")},
+                "roofline": gather_roofline(w, ms, args.workload) if ms is not None else None,
+                "cpu_baseline": None}
+        print(json.dumps(line), flush=True)
+        return
     pipelined = (batch >= PIPELINE_MIN_BATCH and not w.host_table and not args.serial) or args.pipeline
     if args.graph:
         pipelined = False

@@ -80,16 +80,21 @@ struct ColTask {
     int32_t draws_out;    // 1: this column's pieces write the selected slots, starts and weights
 };
 
+// A gather that selects its own windows (FIFO, LIFO or uniform draws): a
+// kernel argument of its own, beside CollectArgs.
+struct DrawArgs {
+    int32_t computed;       // 1: the windows are `draws`, computed per piece; 0: from CollectArgs::idx, start
+    SimpleDraws draws;
+    int64_t* idx_out;       // the draws, written by the pieces of a draws_out column
+    int32_t* start_out;
+    float* w_out;           // ... and weight 1 per draw, when not NULL
+};
+
 struct CollectArgs {
     ColTask col[kMaxLaunchCols];
     int32_t ncols;
-    const int64_t* idx;     // the caller's draws, unless `computed`
+    const int64_t* idx;     // the caller's draws, unless DrawArgs::computed
     const int32_t* start;
-    int32_t computed;       // 1: FIFO, LIFO or uniform draws computed here from `draws`
-    SimpleDraws draws;
-    int64_t* idx_out;       // with `computed`: the draws, written by the pieces of a draws_out column
-    int32_t* start_out;
-    float* w_out;           // ... and weight 1 per draw, when not NULL
     int32_t B;
     int32_t T;
     int32_t L;
@@ -154,8 +159,9 @@ __device__ __forceinline__ int64_t lane_elem(int k) {
 constexpr int64_t kNoWindow = -1;
 constexpr int64_t kBadWindow = -2;
 
-__device__ inline int64_t window_offset(const CollectArgs& a, const ColTask& c, int64_t b) {
-    if (a.computed) return (simple_slot(a.draws, b) * a.T + simple_start(a.draws, b)) * c.E;
+__device__ __forceinline__ int64_t window_offset(const CollectArgs& a, const DrawArgs& g, const ColTask& c,
+                                                 int64_t b) {
+    if (g.computed) return (simple_slot(g.draws, b) * a.T + simple_start(g.draws, b)) * c.E;
     const int64_t i = a.idx[b];
     const int32_t s = a.start[b];
     if (i == -1) return kNoWindow;
@@ -166,10 +172,10 @@ __device__ inline int64_t window_offset(const CollectArgs& a, const ColTask& c, 
 // A gather that selects its own windows writes draw b's slot, start and
 // weight once: from the piece of the draws_out column that holds the
 // window's first element.
-__device__ inline void write_draw(const CollectArgs& a, int64_t b) {
-    a.idx_out[b] = simple_slot(a.draws, b);
-    a.start_out[b] = simple_start(a.draws, b);
-    if (a.w_out) a.w_out[b] = 1.0f;
+__device__ __forceinline__ void write_draw(const DrawArgs& g, int64_t b) {
+    g.idx_out[b] = simple_slot(g.draws, b);
+    g.start_out[b] = simple_start(g.draws, b);
+    if (g.w_out) g.w_out[b] = 1.0f;
 }
 
 // Piece q of a wide column: output elements [q*P, q*P + m) of the column's
@@ -177,7 +183,7 @@ __device__ inline void write_draw(const CollectArgs& a, int64_t b) {
 // window has n >= P elements, so the piece lies in window w0 from element r0
 // on and, if r0 + m > n, runs into window w0 + 1.
 template <int WIDTH, int U>
-__device__ void copy_wide(const CollectArgs& a, const ColTask& c, int64_t q) {
+__device__ void copy_wide(const CollectArgs& a, const DrawArgs& g, const ColTask& c, int64_t q) {
     typedef typename Elem<WIDTH>::type V;
     constexpr int64_t P = (int64_t)kThreads * U;
     const int64_t o0 = q * P;
@@ -186,12 +192,12 @@ __device__ void copy_wide(const CollectArgs& a, const ColTask& c, int64_t q) {
     const int64_t total = (int64_t)a.B * c.n;
     const int64_t m = (total - o0) < P ? (total - o0) : P;
     const bool two = r0 + m > c.n;
-    const int64_t so0 = window_offset(a, c, w0);
-    const int64_t so1 = two ? window_offset(a, c, w0 + 1) : kNoWindow;
+    const int64_t so0 = window_offset(a, g, c, w0);
+    const int64_t so1 = two ? window_offset(a, g, c, w0 + 1) : kNoWindow;
     if (threadIdx.x == 0 && (so0 == kBadWindow || so1 == kBadWindow)) atomicOr(a.status, GEAR_STATUS_BAD_INDEX);
     if (c.draws_out && threadIdx.x == 0) {  // a piece holds at most one window's first element
-        if (r0 == 0) write_draw(a, w0);
-        else if (two) write_draw(a, w0 + 1);
+        if (r0 == 0) write_draw(g, w0);
+        else if (two) write_draw(g, w0 + 1);
     }
     const V* src = reinterpret_cast<const V*>(c.src);
     V* dst = reinterpret_cast<V*>(c.out) + o0;
@@ -228,7 +234,7 @@ __device__ void copy_wide(const CollectArgs& a, const ColTask& c, int64_t q) {
 }
 
 template <int WIDTH, int U>
-__device__ void copy_narrow(const CollectArgs& a, const ColTask& c, int64_t q) {
+__device__ void copy_narrow(const CollectArgs& a, const DrawArgs& g, const ColTask& c, int64_t q) {
     typedef typename Elem<WIDTH>::type V;
     __shared__ int64_t s_off[kThreads];   // source element offset per window, -1 if invalid
     __shared__ int s_bad;
@@ -237,10 +243,10 @@ __device__ void copy_narrow(const CollectArgs& a, const ColTask& c, int64_t q) {
     if (threadIdx.x == 0) s_bad = 0;
     __syncthreads();
     if ((int)threadIdx.x < nb) {
-        const int64_t so = window_offset(a, c, b0 + threadIdx.x);
+        const int64_t so = window_offset(a, g, c, b0 + threadIdx.x);
         s_off[threadIdx.x] = so < 0 ? -1 : so / WIDTH;
         if (so == kBadWindow) s_bad = 1;
-        if (c.draws_out) write_draw(a, b0 + threadIdx.x);
+        if (c.draws_out) write_draw(g, b0 + threadIdx.x);
     }
     __syncthreads();
     if (threadIdx.x == 0 && s_bad) atomicOr(a.status, GEAR_STATUS_BAD_INDEX);
@@ -266,20 +272,20 @@ __device__ void copy_narrow(const CollectArgs& a, const ColTask& c, int64_t q) {
 }
 
 template <int U>
-__global__ __launch_bounds__(kThreads) void collect_kernel(CollectArgs a) {
+__global__ __launch_bounds__(kThreads) void collect_kernel(CollectArgs a, DrawArgs g) {
     const int64_t task = blockIdx.x;
     int j = 0;
     while (j + 1 < a.ncols && a.col[j + 1].task0 <= task) j++;
     const ColTask& c = a.col[j];
     const int64_t q = task - c.task0;
     if (c.wide) {
-        if (c.width == 16) copy_wide<16, U>(a, c, q);
-        else if (c.width == 4) copy_wide<4, U>(a, c, q);
-        else copy_wide<1, U>(a, c, q);
+        if (c.width == 16) copy_wide<16, U>(a, g, c, q);
+        else if (c.width == 4) copy_wide<4, U>(a, g, c, q);
+        else copy_wide<1, U>(a, g, c, q);
     } else {
-        if (c.width == 16) copy_narrow<16, U>(a, c, q);
-        else if (c.width == 4) copy_narrow<4, U>(a, c, q);
-        else copy_narrow<1, U>(a, c, q);
+        if (c.width == 16) copy_narrow<16, U>(a, g, c, q);
+        else if (c.width == 4) copy_narrow<4, U>(a, g, c, q);
+        else copy_narrow<1, U>(a, g, c, q);
     }
 }
 
@@ -299,12 +305,13 @@ int launch_collect(Table* t, const int64_t* d_idx, const int32_t* d_start, const
         CollectArgs a{};
         a.idx = d_idx;
         a.start = d_start;
-        a.computed = draws != nullptr;
+        DrawArgs g{};
+        g.computed = draws != nullptr;
         if (draws) {
-            a.draws = *draws;
-            a.idx_out = idx_out;
-            a.start_out = start_out;
-            a.w_out = w_out;
+            g.draws = *draws;
+            g.idx_out = idx_out;
+            g.start_out = start_out;
+            g.w_out = w_out;
         }
         a.B = B;
         a.T = t->T;
@@ -356,11 +363,11 @@ int launch_collect(Table* t, const int64_t* d_idx, const int32_t* d_start, const
         const unsigned cap = (t->options & GEAR_OPT_GATHER_SHARE_CU) ? kShareLds : kCapLds;
         const unsigned lds = !pinned && tasks >= kCapRounds * kResidentWorkgroups ? cap : 0u;
         if (unroll == kUnrollLarge)
-            hipLaunchKernelGGL(collect_kernel<kUnrollLarge>, dim3((unsigned)tasks), dim3(kThreads), lds, s, a);
+            hipLaunchKernelGGL(collect_kernel<kUnrollLarge>, dim3((unsigned)tasks), dim3(kThreads), lds, s, a, g);
         else if (unroll == kUnrollHost)
-            hipLaunchKernelGGL(collect_kernel<kUnrollHost>, dim3((unsigned)tasks), dim3(kThreads), lds, s, a);
+            hipLaunchKernelGGL(collect_kernel<kUnrollHost>, dim3((unsigned)tasks), dim3(kThreads), lds, s, a, g);
         else
-            hipLaunchKernelGGL(collect_kernel<kUnrollSmall>, dim3((unsigned)tasks), dim3(kThreads), lds, s, a);
+            hipLaunchKernelGGL(collect_kernel<kUnrollSmall>, dim3((unsigned)tasks), dim3(kThreads), lds, s, a, g);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return hip_fail(e, (std::string(who) + ": launch").c_str());
     }
