@@ -1190,6 +1190,10 @@ def main():
               "over more than %d slots, or with the incremental tree, decides per call how to keep its sum tree)"
               % (w.name, gear.GEAR_SMALL_SELECT_MAX_N), file=sys.stderr)
         sys.exit(2)
+    if args.fused and (w.strategies[0] not in (gear.GEAR_FIFO, gear.GEAR_LIFO, gear.GEAR_UNIFORM) or not w.elem_bytes):
+        print("bench.py --fused: only FIFO, LIFO and uniform workloads with columns (%s is not)" % w.name,
+              file=sys.stderr)
+        sys.exit(2)
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
     gear.lib()  # fails loudly if the library is not built
@@ -1207,9 +1211,6 @@ def main():
     # and selection-only workloads, run in order on one stream.
     batch = w.B * w.L * sum(w.elem_bytes)
     if args.fused:
-        if strategy not in (gear.GEAR_FIFO, gear.GEAR_LIFO, gear.GEAR_UNIFORM) or not w.elem_bytes:
-            print("bench.py --fused: only FIFO, LIFO and uniform workloads with columns", file=sys.stderr)
-            sys.exit(2)
         wall, ms = run_fused(t, w, K, W, dev, graph=args.graph, timed_every=1 if batch >= PIPELINE_MIN_BATCH else 4)
         t.close()
         line = {"metric": METRIC, "value": round(w.B * w.L * K / wall, 1), "unit": "trajectory-steps/s",

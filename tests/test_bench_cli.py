@@ -98,3 +98,11 @@ def test_group_of_zero_steps_is_refused():
                        text=True, timeout=120)
     assert r.returncode == 2
     assert "--group" in r.stderr
+
+
+def test_fused_mode_only_for_fifo_lifo_uniform_workloads():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "mat", "--fused"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 2
+    assert "--fused" in r.stderr
+    assert r.stdout.strip() == ""
