@@ -201,8 +201,11 @@ def ceilings():
 
 
 def source_sha(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    """Hash of a source's code: line comments and blank lines left out, so
+    that a comment edit does not invalidate counters taken on the same code."""
+    with open(path) as f:
+        code = [l.split("//", 1)[0].rstrip() for l in f]
+    return hashlib.sha256("\n".join(l for l in code if l).encode()).hexdigest()
 
 
 def profiled_traffic(kernel_key, workload_name):

@@ -16,6 +16,12 @@
 // through its mapped address, so the loads go over the host link without a
 // CPU copy.
 //
+// gear_select_collect runs the same kernel for FIFO, LIFO or uniform draws
+// (Sec. 3.3): instead of reading idx[b] and start[b], each piece computes its
+// windows' draws from the ring state and the seed, and the piece holding a
+// window's first element in the first requested column writes the draw's
+// slot, start and weight.  A step then needs no separate selection launch.
+//
 // Element width per column: 16 bytes when every window source and output
 // address is 16-byte aligned, else 4 bytes when 4-byte aligned, else 1.
 // Sources are aligned when the column base and the step size are, or, for
