@@ -5,8 +5,8 @@ written into its index and start buffers by eager work, and every replay
 must equal the oracle's windows for those draws.
 
 Whole steps (select, collect and, for prioritized and TopK selection, the
-priority update) of the strategies whose selection keeps no decision on the
-host are captured from one table and replayed several times, while a twin
+priority update; or one gear_select_collect call) of the strategies whose
+selection keeps no decision on the host are captured from one table and replayed several times, while a twin
 table runs the same steps eagerly; every replay must give the eager run's
 indices, starts, weights, batches and priorities bit for bit.
 """
@@ -62,8 +62,11 @@ def test_captured_collect_replays_new_draws(pinned):
 # table (4096 slots: selection in one launch, no sum tree).
 DT_SMALL = dataclasses.replace(configs.DT, name="dt-small N=4096 T=100 B=512 L=20", N=4096, T=100,
                                n_insert=4096 + 512)
-STEP_CASES = [(DT_SMALL, gear.GEAR_UNIFORM), (DT_SMALL, gear.GEAR_FIFO), (DT_SMALL, gear.GEAR_LIFO),
-              (configs.TINY, gear.GEAR_PRIORITIZED), (configs.TINY, gear.GEAR_TOPK)]
+STEP_CASES = [(DT_SMALL, gear.GEAR_UNIFORM, False), (DT_SMALL, gear.GEAR_FIFO, False),
+              (DT_SMALL, gear.GEAR_LIFO, False), (configs.TINY, gear.GEAR_PRIORITIZED, False),
+              (configs.TINY, gear.GEAR_TOPK, False),
+              # one gear_select_collect launch per step
+              (DT_SMALL, gear.GEAR_UNIFORM, True), (DT_SMALL, gear.GEAR_FIFO, True), (DT_SMALL, gear.GEAR_LIFO, True)]
 STEPS, REPLAYS = 5, 3
 
 
@@ -75,9 +78,13 @@ def _buffers(w):
             for _ in range(STEPS)]
 
 
-def _steps(t, w, strategy, bufs, newp, stream):
+def _steps(t, w, strategy, bufs, newp, stream, fused=False):
     weights = strategy in (gear.GEAR_PRIORITIZED, gear.GEAR_TOPK)
     for j, (idx, start, wts, outs) in enumerate(bufs):
+        if fused:
+            gear.gear_select_collect(t.handle, strategy, w.B, w.L, gen.select_seed(w.seed, j), idx.data_ptr(),
+                                     start.data_ptr(), wts.data_ptr(), None, [o.data_ptr() for o in outs], stream)
+            continue
         gear.gear_select(t.handle, strategy, w.B, w.L, gen.select_seed(w.seed, j), w.beta, idx.data_ptr(),
                          start.data_ptr(), wts.data_ptr() if weights else None, stream)
         gear.gear_collect(t.handle, idx.data_ptr(), start.data_ptr(), w.B, w.L, None, [o.data_ptr() for o in outs],
@@ -86,9 +93,10 @@ def _steps(t, w, strategy, bufs, newp, stream):
             gear.gear_update_priorities(t.handle, idx.data_ptr(), newp[j].data_ptr(), w.B, stream)
 
 
-@pytest.mark.parametrize("w,strategy", STEP_CASES, ids=["dt-uniform", "dt-fifo", "dt-lifo", "tiny-prioritized",
-                                                        "tiny-topk"])
-def test_captured_steps_replay_like_eager_steps(w, strategy):
+@pytest.mark.parametrize("w,strategy,fused", STEP_CASES,
+                         ids=["dt-uniform", "dt-fifo", "dt-lifo", "tiny-prioritized", "tiny-topk", "dt-uniform-fused",
+                              "dt-fifo-fused", "dt-lifo-fused"])
+def test_captured_steps_replay_like_eager_steps(w, strategy, fused):
     dev = cuda()
     eager_t, graph_t = gpu_table(w), gpu_table(w)
     try:
@@ -99,14 +107,14 @@ def test_captured_steps_replay_like_eager_steps(w, strategy):
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=side, capture_error_mode="relaxed"):
-            _steps(graph_t, w, strategy, graph_b, newp, side.cuda_stream)
+            _steps(graph_t, w, strategy, graph_b, newp, side.cuda_stream, fused)
         scratch = [torch.empty(w.B * w.L * e, dtype=torch.uint8, device=dev) for e in w.elem_bytes]
         for r in range(REPLAYS):
             say("captured steps: %s strategy %d, replay %d" % (w.name, strategy, r))
-            _steps(eager_t, w, strategy, eager_b, newp, torch.cuda.current_stream(dev).cuda_stream)
+            _steps(eager_t, w, strategy, eager_b, newp, torch.cuda.current_stream(dev).cuda_stream, fused)
             g.replay()
             torch.cuda.synchronize()
-            nout = 3 if strategy in (gear.GEAR_PRIORITIZED, gear.GEAR_TOPK) else 2  # weights written or not
+            nout = 3 if fused or strategy in (gear.GEAR_PRIORITIZED, gear.GEAR_TOPK) else 2  # weights written or not
             for j, (a, b) in enumerate(zip(eager_b, graph_b)):
                 for x, y in zip(a[:nout], b[:nout]):
                     np.testing.assert_array_equal(host(x), host(y), err_msg="replay %d step %d" % (r, j))
