@@ -444,6 +444,18 @@ class Table:
                      [o.data_ptr() for o in out], self._stream(stream))
         return out
 
+    def select_collect_fields(self, strategy, B, L, seed, fields=None, weights=False, stream=None):
+        """select_collect with the batch as {name: tensor[B, L, *shape]} views
+        of each column's dtype, as collect_fields returns them."""
+        names = [c.name for c in self.columns] if fields is None else list(fields)
+        ids = [self._index[n] for n in names]
+        idx, start, w, raw = self.select_collect(strategy, B, L, seed, weights=weights, col_ids=ids, stream=stream)
+        res = {}
+        for n, c, r in zip(names, ids, raw):
+            spec = self.columns[c]
+            res[n] = r.view(spec.torch_dtype()).view((B, L) + spec.shape)
+        return idx, start, w, res
+
     def select_collect(self, strategy, B, L, seed, weights=False, col_ids=None, stream=None):
         """FIFO, LIFO or uniform selection and its gather in one launch:
         (idx, start, w, list of uint8 tensors [B, L*E_c]), equal to select()

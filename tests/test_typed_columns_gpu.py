@@ -67,6 +67,18 @@ def test_typed_table_collect_fields_matches_oracle():
         assert list(part) == ["reward", "obs"]
         assert torch.equal(part["reward"], batch["reward"])
         assert torch.equal(part["obs"].view(torch.uint8), batch["obs"].view(torch.uint8))
+        # Uniform selection inside the gather launch hands out the same typed views.
+        uidx, ustart, _, ubatch = t.select_collect_fields(gear.GEAR_UNIFORM, B, L, seed + 1, fields=["action", "obs"])
+        assert list(ubatch) == ["action", "obs"]
+        assert tuple(ubatch["obs"].shape) == (B, L, 8, 64) and ubatch["action"].dtype == torch.int32
+        st, oidx, ostart, _ = store.select(oracle.UNIFORM, B, L, seed + 1)
+        assert st == oracle.OK
+        np.testing.assert_array_equal(host(uidx), oidx)
+        np.testing.assert_array_equal(host(ustart), ostart)
+        _, ref = store.collect(oidx, ostart, L)
+        assert torch.equal(ubatch["action"].cpu().view(torch.uint8).reshape(-1),
+                           torch.from_numpy(ref[1]).reshape(-1))
+        assert torch.equal(ubatch["obs"].cpu().view(torch.uint8).reshape(-1), torch.from_numpy(ref[0]).reshape(-1))
         assert t.sync() == 0
     finally:
         t.close()
