@@ -56,6 +56,8 @@ def test_argument_validation_without_device():
     assert "capacity" in gear.gear_last_error()
     assert lib.gear_select(None, 3, 1, 1, 0, ctypes.c_float(0), None, None, None, None) == gear.GEAR_E_INVAL
     assert lib.gear_collect(None, None, None, 1, 1, None, 1, None, None) == gear.GEAR_E_INVAL
+    assert lib.gear_select_collect(None, 0, 1, 1, 0, None, None, None, None, 1, None, None) == gear.GEAR_E_INVAL
+    assert "gear_select_collect" in gear.gear_last_error()
     assert lib.gear_update_priorities(None, None, None, 1, None) == gear.GEAR_E_INVAL
     assert lib.gear_insert(None, 1, None, None, None) == gear.GEAR_E_INVAL
     assert lib.gear_table_sync(None, None, None) == gear.GEAR_E_INVAL
