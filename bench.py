@@ -20,6 +20,7 @@ sample of the same workload.
   python bench.py --ceilings      # HBM read / write / copy rates of plain kernels
 """
 import argparse
+import dataclasses
 import ctypes
 import hashlib
 import json
@@ -99,6 +100,8 @@ def parse():
     ap.add_argument("--graph", action="store_true",
                     help="capture the timed steps into one HIP graph and replay it (steps in order on one stream; "
                          "only workloads whose calls replay correctly from a capture)")
+    ap.add_argument("--strategy", choices=["fifo", "lifo", "uniform", "prioritized", "topk"],
+                    help="select with this one of the workload's strategies instead of its first")
     ap.add_argument("--fused", action="store_true",
                     help="FIFO, LIFO and uniform workloads: each step is one gear_select_collect launch "
                          "(selection computed inside the gather)")
@@ -1186,6 +1189,13 @@ def main():
     from paper_2310_05205_amd import gear
 
     w = workload(args.workload)
+    if args.strategy:
+        code = {"fifo": 0, "lifo": 1, "uniform": 2, "prioritized": 3, "topk": 4}[args.strategy]
+        if code not in w.strategies:
+            print("bench.py --strategy: %s is not one of the %s workload's strategies" % (args.strategy, w.name),
+                  file=sys.stderr)
+            sys.exit(2)
+        w = dataclasses.replace(w, strategies=(code,) + tuple(x for x in w.strategies if x != code))
     opts = (gear.GEAR_OPT_INCREMENTAL_TREE if args.incremental else 0) | \
         (gear.GEAR_OPT_IS_GLOBAL_MIN if args.global_min else 0)
     if args.graph and not capturable(w, opts):
